@@ -1,0 +1,71 @@
+/*
+ * oracle.h -- CPU oracle for PruneKV (VisCache, "PruneKV: Layer-Aware Visual KV
+ * Cache Compression", Sec. 3.2 and Appendix B, Algorithm 1).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This is a plain, slow, single-threaded C
+ * implementation in double precision, used to check the GPU library.  Only the
+ * test suite, the smoke check and the benchmark's CPU-baseline leg may load it;
+ * the product path never calls it, and it shares no source with the GPU path.
+ *
+ * bf16 values are passed as uint16 bit patterns.  All functions are reentrant
+ * (no global state) so callers may run independent units on several threads.
+ */
+#ifndef PRUNEKV_ORACLE_H
+#define PRUNEKV_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Layer budgets: Eq. (parabolic) with the normalisation to sum h*m that
+ * follows it, the retention-ratio composition RR = p*q*(h/L)*m of the
+ * implementation details (p = 1), and Alg. 1 Step 1 (the top-q cut).
+ * Inputs: L layers, n visual tokens, overall retention rr in (0,1], h_param
+ * (0 selects round(0.75 L)), mean budget m in (0,1].
+ * Outputs: k[L] kept tokens per layer (0 beyond h), *n_surv (tokens that
+ * survive the top-q cut), *h_out, b_out[L] (normalised proportions, may be
+ * NULL), *q_out (may be NULL).  Returns 0, or -1 on invalid parameters. */
+int orc_budget(int32_t L, int32_t n, double rr, int32_t h_param, double m,
+               int32_t *k, int32_t *n_surv, int32_t *h_out, double *b_out, double *q_out);
+
+/* Window score of one (sequence, layer, kv head) unit, Eq. (token_score) read
+ * as: for every query row r of the G*W window rows, the softmax over the n
+ * visual keys of (bf16(q_r) . k_v) / sqrt(d); S[v] = sum over rows.
+ * K: bf16 [n][d]; Q: fp32 [G*W][d] (rounded to bf16 first).  S: fp64 [n]. */
+void orc_scores_unit(int32_t n, int32_t d, int32_t rows, const uint16_t *K, const float *Q,
+                     double *S);
+
+/* Keep / drop partition (Alg. 1 Step 1 and Step 3): order tokens by
+ * (score descending, index ascending); kept = the first k, drop = the next
+ * n_surv - k; the rest are discarded.  Both lists are written ascending. */
+void orc_select(int32_t n, const float *score, int32_t k, int32_t n_surv,
+                int32_t *kept, int32_t *drop);
+
+/* Key pruning: K_out[j] = K[kept[j]] (bit copy of d bf16 values). */
+void orc_gather(int32_t d, int32_t k, const int32_t *kept, const uint16_t *K, uint16_t *K_out);
+
+/* Value fusion, Eq. (redistribution) and Eq. (weight_fusion):
+ * Phi = row-softmax(V_k V_d^T / tau); V_new = mu V_k + (1 - mu) Phi V_d.
+ * V: bf16 [n][d] rows of the unit; kept[k], drop[r] index it.
+ * With k == 0 nothing is written; with r == 0, V_new = V_k.
+ * out: fp64 [k][d]. */
+void orc_fuse(int32_t d, int32_t k, int32_t r, const uint16_t *V, const int32_t *kept,
+              const int32_t *drop, double tau, double mu, double *out);
+
+/* Decode attention of one query over one cache (Sec. 2, decoding):
+ * out = sum_t softmax_t(scale * q . K_t) V_t.  q: bf16 [d]; K, V: bf16 [rows][d];
+ * out: fp64 [d]. */
+void orc_attend(int32_t d, int32_t rows, const uint16_t *q, const uint16_t *K, const uint16_t *V,
+                double scale, double *out);
+
+/* One LAYER_HEAD unit end to end: score -> select -> gather -> fuse.
+ * S32 (may be NULL) receives the fp32 scores used for the ranking. */
+void orc_prune_unit(int32_t n, int32_t d, int32_t rows, const uint16_t *K, const uint16_t *V,
+                    const float *Q, int32_t k, int32_t n_surv, double tau, double mu,
+                    int32_t *kept, int32_t *drop, uint16_t *K_out, double *V_out, float *S32);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
