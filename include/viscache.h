@@ -1,0 +1,215 @@
+/*
+ * viscache.h -- C ABI of libviscache, a gfx950 (MI355X) implementation of
+ * PruneKV, the visual KV-cache compression step of VisCache (Sec. 3.2,
+ * "PruneKV: Layer-Aware Visual KV Cache Compression", and Appendix B,
+ * Algorithm 1), plus decode attention over the compressed cache (Sec. 2,
+ * "VLLM Decoding").
+ *
+ * Conventions for every entry point
+ *   - Plain C types only.  Device pointers are addresses returned by the HIP
+ *     allocator (or by a framework that uses it); host pointers are ordinary
+ *     process memory.  Each argument says which one it is.
+ *   - The caller owns every buffer.  The library never allocates or frees
+ *     device memory, never synchronises a stream and keeps no mutable global
+ *     state: calls on different streams with different buffers may overlap.
+ *   - Sizes of outputs and of the workspace come from the host-only query
+ *     functions below, so the device path needs no device-to-host copy.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     Device work is enqueued asynchronously on it.
+ *   - Every argument and shape check runs on the host before anything is
+ *     enqueued; on error nothing is enqueued and the status says why.
+ *     VC_ERR_HIP reports a failed launch.  Faults inside kernels surface at
+ *     the caller's next synchronisation, as for any HIP kernel.
+ *   - Inputs must be finite; non-finite values give unspecified results.
+ *   - bf16 means IEEE binary32 truncated to its upper 16 bits (bfloat16),
+ *     stored as 2-byte values.
+ */
+#ifndef VISCACHE_H
+#define VISCACHE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  VC_OK = 0,
+  VC_ERR_ARG = 1,         /* null pointer, bad enum or out-of-range scalar */
+  VC_ERR_SHAPE = 2,       /* inconsistent or unsupported shape */
+  VC_ERR_BUDGET = 3,      /* retention / h / m give no valid budget (e.g. q > 1) */
+  VC_ERR_WORKSPACE = 4,   /* workspace missing or smaller than required */
+  VC_ERR_UNSUPPORTED = 5, /* shape outside what the kernels are built for */
+  VC_ERR_HIP = 6          /* a HIP runtime call or launch failed */
+} vc_status;
+
+/* Which score ranks the tokens of a layer (Sec. "Ablation on Shared vs.
+ * Layer-Specific Visual Token Ranking").
+ *   LAYER_HEAD: every (layer, kv head) ranks by its own window score.
+ *   GLOBAL:     one shared score per token, summed over all L layers and all
+ *               kv heads; every layer and head keeps the top-k_l of it. */
+typedef enum { VC_RANK_LAYER_HEAD = 0, VC_RANK_GLOBAL = 1 } vc_rank_mode;
+
+/* Method parameters.  Defaults (viscache_default_params) are the paper's fixed
+ * hyper-parameters from Sec. 4, Implementation Details: h = 3/4 L, m = 0.75,
+ * tau = 1.0, mu = 0.7. */
+typedef struct {
+  double retention; /* overall retention ratio RR in (0, 1]; RR = q*(h/L)*m, so
+                       the token-level ratio is q = RR / ((h/L) m), and q > 1 is
+                       VC_ERR_BUDGET.  The totals satisfy
+                       sum_l k_l = floor(RR*L*n + 0.5) per sequence. */
+  int32_t h;        /* truncation layer in [2, L]; layers past h are evicted.
+                       0 selects floor(0.75 L + 0.5). */
+  double m;         /* mean layer budget in (0, 1] (normalisation target h*m
+                       of Eq. (parabolic)). */
+  float tau;        /* temperature of Eq. (redistribution), > 0 */
+  float mu;         /* fusion weight of Eq. (weight_fusion), in [0, 1] */
+  int32_t rank_mode;  /* vc_rank_mode */
+  int32_t v_out_fp32; /* 0: fused values stored as bf16; 1: stored as fp32 */
+} vc_params;
+
+/* Problem shape.  L layers, Hq query heads, Hkv kv heads (Hq % Hkv == 0;
+ * query head hq reads kv head hq / (Hq/Hkv)), head dim d in {64, 128},
+ * W window queries per head, B sequences with n_vis[b] visual tokens each. */
+typedef struct {
+  int32_t B, L, Hq, Hkv, d, W;
+  const int32_t *n_vis; /* HOST array [B]; each entry in [0, 32768] */
+} vc_shape;
+
+/* Fill *p with the defaults above and the given retention. */
+void viscache_default_params(vc_params *p, double retention);
+
+/* Host only.  Layer budgets, Eq. (parabolic) normalised to h*m, and the
+ * top-q survivor count of Algorithm 1 Step 1:
+ *   k[b*L + l]      tokens kept in layer l of sequence b (0 for l >= h),
+ *   n_surv[b*L + l] tokens that survive the top-q cut (same for every l),
+ *   *h_out          the truncation layer used (may be NULL).
+ * Returns VC_ERR_BUDGET for parameters without a valid budget. */
+vc_status viscache_budget(const vc_shape *shape, const vc_params *params, int32_t *k,
+                          int32_t *n_surv, int32_t *h_out);
+
+/* Host only.  Output row offsets: rows[l*(B+1) + b] = sum_{b' < b} Hkv*k[b'*L+l]
+ * for b = 0..B, so layer l's outputs hold rows[l*(B+1)+B] rows.  `rows` is a
+ * HOST array of L*(B+1) entries. */
+vc_status viscache_out_rows(const vc_shape *shape, const vc_params *params, int64_t *rows);
+
+/* Host only.  Bytes of device workspace viscache_prune needs (0 on error). */
+size_t viscache_prune_workspace_bytes(const vc_shape *shape, const vc_params *params);
+
+/* Host only, diagnostic.  Byte offsets inside the prune workspace where
+ * viscache_prune leaves its fp32 window scores once the call has completed:
+ *   *scores_off: [Ls][sum_b Hkv*n_b], Ls = h (LAYER_HEAD) or L (GLOBAL), the
+ *                score of token v of (layer l, sequence b, kv head g) at
+ *                l*(sum_b Hkv*n_b) + off_b*Hkv + g*n_b + v;
+ *   *shared_off: [sum_b n_b] shared scores (GLOBAL), token v of b at off_b + v;
+ *                set to (size_t)-1 in LAYER_HEAD mode.
+ * The contents stay valid until the workspace is reused. */
+vc_status viscache_prune_score_offsets(const vc_shape *shape, const vc_params *params,
+                                       size_t *scores_off, size_t *shared_off);
+
+/* Buffers of one viscache_prune call.  Every member is a HOST array of L
+ * DEVICE pointers, one per layer l.
+ *   k_in[l], v_in[l]: bf16 visual keys / values of layer l, packed over
+ *       sequences: row (b, g, v) at off_b*Hkv + g*n_b + v with
+ *       off_b = sum_{b'<b} n_{b'}; each row holds d values.
+ *   q_win[l]: fp32 window queries [B][Hq][W][d].  They enter the score
+ *       contraction rounded to bf16 (round to nearest even).
+ *   k_out[l]: bf16 kept keys, bit copies of the input rows; v_out[l]: fused
+ *       values, bf16 or fp32 (vc_params.v_out_fp32); idx_out[l]: int32 token
+ *       index (0..n_b-1) of every kept row.  Output row (b, g, j) sits at
+ *       rows[l*(B+1)+b] + g*k[b*L+l] + j, rows ascending in token index.
+ *       Layers l >= h have no rows; their pointers may be NULL.
+ *   drop_out: may be NULL.  Otherwise drop_out[l] receives, per (b, g), the
+ *       r = n_surv - k token indices whose values were fused (ascending),
+ *       at dropped-row offset sum_{b'<b} Hkv*r_{b',l} + g*r_{b,l}.
+ * Input buffers are read only; outputs must not overlap inputs. */
+typedef struct {
+  const void *const *k_in;
+  const void *const *v_in;
+  const float *const *q_win;
+  void *const *k_out;
+  void *const *v_out;
+  int32_t *const *idx_out;
+  int32_t *const *drop_out;
+} vc_prune_io;
+
+/* Device, asynchronous.  PruneKV over all layers and sequences (Algorithm 1):
+ * window scores (Eq. (token_score), read as the attention of the W window
+ * queries, softmax over the n_b visual keys with scale 1/sqrt(d), summed over
+ * the Hq/Hkv query heads of each kv head), budgets as viscache_budget, the
+ * keep set (top-k_l) and drop set (ranks k_l+1..n_surv) from one ranking
+ * ordered by (score descending, token index ascending), key pruning, and
+ * value fusion V_new = mu V_k + (1-mu) softmax(V_k V_d^T / tau) V_d
+ * (Eq. (redistribution), Eq. (weight_fusion)); with no dropped or no kept
+ * rows the kept values are copied unchanged.
+ * `workspace` is a DEVICE buffer of at least viscache_prune_workspace_bytes
+ * bytes, 256-byte aligned; its contents on entry do not matter. */
+vc_status viscache_prune(const vc_shape *shape, const vc_params *params, const vc_prune_io *io,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+/* Number of events viscache_prune_staged records. */
+#define VC_PRUNE_EVENTS 7
+
+/* Device, asynchronous.  viscache_prune with stage timing: `events` is a HOST
+ * array of VC_PRUNE_EVENTS hipEvent_t handles (passed as void*) created by the
+ * caller; event i is recorded on `stream` before stage i and the last one
+ * after the final stage.  Stages: 0 plan upload, 1 score row statistics,
+ * 2 score column sums, 3 shared-score reduction (empty in LAYER_HEAD mode),
+ * 4 keep/drop selection, 5 key gather and value fusion.  events == NULL
+ * behaves exactly as viscache_prune. */
+vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params,
+                                const vc_prune_io *io, void *workspace, size_t workspace_bytes,
+                                void *stream, void *const *events);
+
+/* ---- decode over a (compressed) cache ------------------------------------ */
+
+/* Decode shape: L layers, B sequences, Hq query heads, Hkv kv heads, head dim
+ * d in {64, 128}, Hq/Hkv <= 16. */
+typedef struct {
+  int32_t B, L, Hq, Hkv, d;
+} vc_decode_shape;
+
+/* Cache pool for decode.  All layers' caches live in one pair of DEVICE bf16
+ * row pools k_pool / v_pool (d values per row).  Unit u = (l*B + b)*Hkv + g
+ * (layer l, sequence b, kv head g) owns the contiguous rows
+ * [row_off[u], row_off[u] + cap[u]) of both pools and currently holds len[u]
+ * rows.  row_off (int64), cap and len (int32) are DEVICE arrays of L*B*Hkv
+ * entries; the blocks of different units must not overlap. */
+typedef struct {
+  void *k_pool;
+  void *v_pool;
+  const int64_t *row_off;
+  const int32_t *cap;
+  int32_t *len;
+} vc_cache;
+
+/* Host only.  Workspace bytes viscache_decode_attn needs for caches of at most
+ * max_rows rows per (layer, sequence, kv head). */
+size_t viscache_decode_workspace_bytes(const vc_decode_shape *shape, int64_t max_rows);
+
+/* Device, asynchronous.  Appends one key and one value row per unit
+ * (Sec. 2, decoding: K <- concat[K, h_t W_K], V <- concat[V, h_t W_V]) at
+ * row row_off[u] + len[u] and then increments len[u].  k_new, v_new: DEVICE bf16
+ * [L][B][Hkv][d].  A full cache (len == cap) is left unchanged and its length
+ * is not incremented. */
+vc_status viscache_append_kv(const vc_decode_shape *shape, const vc_cache *cache,
+                             const void *k_new, const void *v_new, void *stream);
+
+/* Device, asynchronous.  Decode attention of one new token per sequence and
+ * layer: out[l][b][hq] = softmax_t(scale * q[l][b][hq] . K_t) V_t over the
+ * len rows of (l, b, hq / (Hq/Hkv)).  q: DEVICE bf16 [L][B][Hq][d]; out:
+ * DEVICE fp32 [L][B][Hq][d]; a cache of length 0 gives zeros.  `workspace`:
+ * DEVICE, at least viscache_decode_workspace_bytes(shape, max_rows) bytes,
+ * where max_rows bounds every len; 256-byte aligned. */
+vc_status viscache_decode_attn(const vc_decode_shape *shape, const vc_cache *cache, const void *q,
+                               float *out, float scale, int64_t max_rows, void *workspace,
+                               size_t workspace_bytes, void *stream);
+
+/* Static text for a status code. */
+const char *viscache_strerror(vc_status s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VISCACHE_H */

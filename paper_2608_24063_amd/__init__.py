@@ -1,0 +1,200 @@
+"""Python binding of libviscache (PruneKV on MI355X / gfx950).
+
+Thin ctypes layer over the C ABI declared in ``include/viscache.h``: the same
+entry-point names, argument marshalling only.  Every step of the computation
+runs in the library's HIP kernels; PyTorch only supplies device memory and the
+current stream.  If the shared library has not been built, loading fails
+loudly -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libviscache.so")
+
+VC_OK, VC_ERR_ARG, VC_ERR_SHAPE, VC_ERR_BUDGET, VC_ERR_WORKSPACE, VC_ERR_UNSUPPORTED, VC_ERR_HIP = range(7)
+VC_RANK_LAYER_HEAD, VC_RANK_GLOBAL = 0, 1
+
+P = ctypes.POINTER
+c_i32, c_i64, c_f32, c_f64, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_void_p
+
+
+class vc_params(ctypes.Structure):
+    _fields_ = [("retention", c_f64), ("h", c_i32), ("m", c_f64), ("tau", c_f32), ("mu", c_f32),
+                ("rank_mode", c_i32), ("v_out_fp32", c_i32)]
+
+
+class vc_shape(ctypes.Structure):
+    _fields_ = [("B", c_i32), ("L", c_i32), ("Hq", c_i32), ("Hkv", c_i32), ("d", c_i32),
+                ("W", c_i32), ("n_vis", P(c_i32))]
+
+
+class vc_prune_io(ctypes.Structure):
+    _fields_ = [("k_in", P(c_vp)), ("v_in", P(c_vp)), ("q_win", P(c_vp)), ("k_out", P(c_vp)),
+                ("v_out", P(c_vp)), ("idx_out", P(c_vp)), ("drop_out", P(c_vp))]
+
+
+class vc_decode_shape(ctypes.Structure):
+    _fields_ = [("B", c_i32), ("L", c_i32), ("Hq", c_i32), ("Hkv", c_i32), ("d", c_i32)]
+
+
+class vc_cache(ctypes.Structure):
+    _fields_ = [("k_pool", c_vp), ("v_pool", c_vp), ("row_off", c_vp), ("cap", c_vp), ("len", c_vp)]
+
+
+class VisCacheError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {strerror(status)} (status {status})")
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library.  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: run __graft_entry__.build() first")
+        L = ctypes.CDLL(LIB_PATH)
+        L.viscache_default_params.argtypes = [P(vc_params), c_f64]
+        L.viscache_default_params.restype = None
+        L.viscache_budget.argtypes = [P(vc_shape), P(vc_params), P(c_i32), P(c_i32), P(c_i32)]
+        L.viscache_out_rows.argtypes = [P(vc_shape), P(vc_params), P(c_i64)]
+        L.viscache_prune_workspace_bytes.argtypes = [P(vc_shape), P(vc_params)]
+        L.viscache_prune_workspace_bytes.restype = ctypes.c_size_t
+        L.viscache_prune_score_offsets.argtypes = [P(vc_shape), P(vc_params), P(ctypes.c_size_t),
+                                                   P(ctypes.c_size_t)]
+        L.viscache_prune.argtypes = [P(vc_shape), P(vc_params), P(vc_prune_io), c_vp, ctypes.c_size_t, c_vp]
+        L.viscache_prune_staged.argtypes = [P(vc_shape), P(vc_params), P(vc_prune_io), c_vp, ctypes.c_size_t,
+                                            c_vp, P(c_vp)]
+        L.viscache_decode_workspace_bytes.argtypes = [P(vc_decode_shape), c_i64]
+        L.viscache_decode_workspace_bytes.restype = ctypes.c_size_t
+        L.viscache_append_kv.argtypes = [P(vc_decode_shape), P(vc_cache), c_vp, c_vp, c_vp]
+        L.viscache_decode_attn.argtypes = [P(vc_decode_shape), P(vc_cache), c_vp, c_vp, c_f32, c_i64,
+                                           c_vp, ctypes.c_size_t, c_vp]
+        L.viscache_strerror.argtypes = [c_i32]
+        L.viscache_strerror.restype = ctypes.c_char_p
+        for name in ("viscache_budget", "viscache_out_rows", "viscache_prune", "viscache_prune_score_offsets",
+                     "viscache_prune_staged",
+                     "viscache_append_kv", "viscache_decode_attn"):
+            getattr(L, name).restype = c_i32
+        _lib = L
+    return _lib
+
+
+def strerror(status: int) -> str:
+    return lib().viscache_strerror(status).decode()
+
+
+def _check(status: int, what: str) -> None:
+    if status != VC_OK:
+        raise VisCacheError(status, what)
+
+
+# ---- parameter / shape construction -----------------------------------------
+
+def make_params(retention: float, h: int = 0, m: float = 0.75, tau: float = 1.0, mu: float = 0.7,
+                rank_mode: int = VC_RANK_LAYER_HEAD, v_out_fp32: bool = False) -> vc_params:
+    p = vc_params()
+    lib().viscache_default_params(ctypes.byref(p), retention)
+    p.h, p.m, p.tau, p.mu, p.rank_mode, p.v_out_fp32 = h, m, tau, mu, rank_mode, int(v_out_fp32)
+    return p
+
+
+def make_shape(B: int, L: int, Hq: int, Hkv: int, d: int, W: int, n_vis) -> vc_shape:
+    arr = (c_i32 * B)(*[int(x) for x in n_vis])
+    s = vc_shape(B, L, Hq, Hkv, d, W, ctypes.cast(arr, P(c_i32)))
+    s._keep = arr  # keep the host array alive with the struct
+    return s
+
+
+# ---- the C entry points, same names ------------------------------------------
+
+def viscache_budget(shape: vc_shape, params: vc_params):
+    """Returns (k[B*L], n_surv[B*L], h) as Python lists."""
+    n = shape.B * shape.L
+    k, ns, h = (c_i32 * n)(), (c_i32 * n)(), c_i32()
+    _check(lib().viscache_budget(ctypes.byref(shape), ctypes.byref(params), k, ns, ctypes.byref(h)),
+           "viscache_budget")
+    return list(k), list(ns), h.value
+
+
+def viscache_out_rows(shape: vc_shape, params: vc_params):
+    rows = (c_i64 * (shape.L * (shape.B + 1)))()
+    _check(lib().viscache_out_rows(ctypes.byref(shape), ctypes.byref(params), rows), "viscache_out_rows")
+    return list(rows)
+
+
+def viscache_prune_workspace_bytes(shape: vc_shape, params: vc_params) -> int:
+    return int(lib().viscache_prune_workspace_bytes(ctypes.byref(shape), ctypes.byref(params)))
+
+
+def viscache_prune_score_offsets(shape: vc_shape, params: vc_params):
+    """(scores_off, shared_off or None): byte offsets of the scores in the workspace."""
+    a, b = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(lib().viscache_prune_score_offsets(ctypes.byref(shape), ctypes.byref(params), ctypes.byref(a),
+                                              ctypes.byref(b)), "viscache_prune_score_offsets")
+    return a.value, (None if b.value == ctypes.c_size_t(-1).value else b.value)
+
+
+def _ptrs(seq):
+    arr = (c_vp * len(seq))(*[int(x) if x else None for x in seq])
+    return arr
+
+
+VC_PRUNE_EVENTS = 7
+
+
+def _io(k_in, v_in, q_win, k_out, v_out, idx_out, drop_out):
+    arrs = [_ptrs(x) for x in (k_in, v_in, q_win, k_out, v_out, idx_out)]
+    drop = _ptrs(drop_out) if drop_out is not None else None
+    io = vc_prune_io(*[ctypes.cast(a, P(c_vp)) for a in arrs],
+                     ctypes.cast(drop, P(c_vp)) if drop is not None else None)
+    io._keep = (arrs, drop)
+    return io
+
+
+def viscache_prune(shape: vc_shape, params: vc_params, k_in, v_in, q_win, k_out, v_out, idx_out,
+                   workspace: int, workspace_bytes: int, stream: int, drop_out=None) -> None:
+    """k_in ... idx_out, drop_out: sequences of L device addresses (ints, 0 for none)."""
+    io = _io(k_in, v_in, q_win, k_out, v_out, idx_out, drop_out)
+    _check(lib().viscache_prune(ctypes.byref(shape), ctypes.byref(params), ctypes.byref(io),
+                                workspace, workspace_bytes, stream), "viscache_prune")
+
+
+def viscache_prune_staged(shape: vc_shape, params: vc_params, k_in, v_in, q_win, k_out, v_out, idx_out,
+                          workspace: int, workspace_bytes: int, stream: int, events, drop_out=None) -> None:
+    """As viscache_prune; `events` = VC_PRUNE_EVENTS raw hipEvent_t handles (ints)."""
+    io = _io(k_in, v_in, q_win, k_out, v_out, idx_out, drop_out)
+    ev = (c_vp * VC_PRUNE_EVENTS)(*[int(e) for e in events])
+    _check(lib().viscache_prune_staged(ctypes.byref(shape), ctypes.byref(params), ctypes.byref(io),
+                                       workspace, workspace_bytes, stream, ev), "viscache_prune_staged")
+
+
+def viscache_decode_workspace_bytes(shape: vc_decode_shape, max_rows: int) -> int:
+    return int(lib().viscache_decode_workspace_bytes(ctypes.byref(shape), max_rows))
+
+
+def viscache_append_kv(shape: vc_decode_shape, cache: vc_cache, k_new: int, v_new: int, stream: int) -> None:
+    _check(lib().viscache_append_kv(ctypes.byref(shape), ctypes.byref(cache), k_new, v_new, stream),
+           "viscache_append_kv")
+
+
+def viscache_decode_attn(shape: vc_decode_shape, cache: vc_cache, q: int, out: int, scale: float,
+                         max_rows: int, workspace: int, workspace_bytes: int, stream: int) -> None:
+    _check(lib().viscache_decode_attn(ctypes.byref(shape), ctypes.byref(cache), q, out, scale, max_rows,
+                                      workspace, workspace_bytes, stream), "viscache_decode_attn")
+
+
+def viscache_strerror(status: int) -> str:
+    return strerror(status)
+
+
+EXPORTED = ("viscache_default_params", "viscache_budget", "viscache_out_rows",
+            "viscache_prune_workspace_bytes", "viscache_prune_score_offsets", "viscache_prune",
+            "viscache_prune_staged", "viscache_decode_workspace_bytes",
+            "viscache_append_kv", "viscache_decode_attn", "viscache_strerror")

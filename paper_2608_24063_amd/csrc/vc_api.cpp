@@ -1,0 +1,361 @@
+// vc_api.cpp -- the C ABI of libviscache (include/viscache.h): argument
+// checks, budgets, workspace layout, and the launch sequence of one PruneKV
+// call (Algorithm 1) and of one decode step.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "../../include/viscache.h"
+#include "vc_budget.h"
+#include "vc_internal.h"
+
+using namespace vc;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+// Everything derived from (shape, params) on the host.
+struct Layout {
+  int32_t B, L, Hq, Hkv, d, W, G, R, h, Ls, mode, vfp32;
+  int32_t nqg, nks, ncol, nfuse, nmax;
+  int64_t Ntot;
+  std::vector<int32_t> n, k, ns;       // n[B], k[B*L], ns[B*L]
+  std::vector<int64_t> toff, orow, drow;
+  // workspace regions (byte offsets)
+  size_t off_plan, plan_bytes, off_qbf, off_part, off_S, off_gs, off_drop, total;
+  // offsets inside the plan blob
+  size_t p_lp, p_nb, p_toff, p_kk, p_ns, p_orow, p_drow;
+};
+
+vc_status check_shape(const vc_shape *s) {
+  if (!s || !s->n_vis) return VC_ERR_ARG;
+  if (s->B < 1 || s->L < 2 || s->Hq < 1 || s->Hkv < 1 || s->W < 1) return VC_ERR_SHAPE;
+  if (s->Hq % s->Hkv != 0) return VC_ERR_SHAPE;
+  if (s->d != 64 && s->d != 128) return VC_ERR_UNSUPPORTED;
+  if ((int64_t)(s->Hq / s->Hkv) * s->W > 1024) return VC_ERR_UNSUPPORTED;
+  for (int32_t b = 0; b < s->B; ++b)
+    if (s->n_vis[b] < 0 || s->n_vis[b] > kMaxTokens) return s->n_vis[b] < 0 ? VC_ERR_SHAPE : VC_ERR_UNSUPPORTED;
+  return VC_OK;
+}
+
+vc_status check_params(const vc_params *p, int32_t L) {
+  if (!p) return VC_ERR_ARG;
+  if (!(p->retention > 0.0 && p->retention <= 1.0)) return VC_ERR_BUDGET;
+  if (!(p->m > 0.0 && p->m <= 1.0)) return VC_ERR_BUDGET;
+  if (p->h != 0 && (p->h < 2 || p->h > L)) return VC_ERR_BUDGET;
+  if (!(p->tau > 0.f) || !std::isfinite(p->tau)) return VC_ERR_ARG;
+  if (!(p->mu >= 0.f && p->mu <= 1.f)) return VC_ERR_ARG;
+  if (p->rank_mode != VC_RANK_LAYER_HEAD && p->rank_mode != VC_RANK_GLOBAL) return VC_ERR_ARG;
+  if (p->v_out_fp32 != 0 && p->v_out_fp32 != 1) return VC_ERR_ARG;
+  return VC_OK;
+}
+
+vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
+  vc_status st = check_shape(s);
+  if (st != VC_OK) return st;
+  st = check_params(p, s->L);
+  if (st != VC_OK) return st;
+  y.B = s->B; y.L = s->L; y.Hq = s->Hq; y.Hkv = s->Hkv; y.d = s->d; y.W = s->W;
+  y.G = s->Hq / s->Hkv;
+  y.R = y.G * y.W;
+  y.mode = p->rank_mode;
+  y.vfp32 = p->v_out_fp32;
+  y.n.assign(s->n_vis, s->n_vis + s->B);
+  y.k.assign((size_t)y.B * y.L, 0);
+  y.ns.assign((size_t)y.B * y.L, 0);
+  y.h = 0;
+  for (int32_t b = 0; b < y.B; ++b) {
+    int32_t nsv = 0, hu = 0;
+    if (!budget_one(y.L, y.n[b], p->retention, p->h, p->m, &y.k[(size_t)b * y.L], &nsv, &hu))
+      return VC_ERR_BUDGET;
+    for (int32_t l = 0; l < y.L; ++l) y.ns[(size_t)b * y.L + l] = nsv;
+    y.h = hu;
+  }
+  y.Ls = y.mode == VC_RANK_GLOBAL ? y.L : y.h;
+  y.toff.assign(y.B + 1, 0);
+  for (int32_t b = 0; b < y.B; ++b) y.toff[b + 1] = y.toff[b] + y.n[b];
+  y.Ntot = y.toff[y.B];
+  y.orow.assign((size_t)y.L * (y.B + 1), 0);
+  y.drow.assign((size_t)y.L * (y.B + 1), 0);
+  int32_t kmax = 0;
+  for (int32_t l = 0; l < y.L; ++l)
+    for (int32_t b = 0; b < y.B; ++b) {
+      const int32_t kk = y.k[(size_t)b * y.L + l];
+      const int32_t rr = l < y.h ? y.ns[(size_t)b * y.L + l] - kk : 0;
+      y.orow[(size_t)l * (y.B + 1) + b + 1] = y.orow[(size_t)l * (y.B + 1) + b] + (int64_t)y.Hkv * kk;
+      y.drow[(size_t)l * (y.B + 1) + b + 1] = y.drow[(size_t)l * (y.B + 1) + b] + (int64_t)y.Hkv * rr;
+      kmax = std::max(kmax, kk);
+    }
+  y.nmax = *std::max_element(y.n.begin(), y.n.end());
+  const int64_t units = (int64_t)y.Ls * y.B * y.Hkv;
+  y.nqg = (y.R + kStatsRows - 1) / kStatsRows;
+  const int64_t base = std::max<int64_t>(1, units * y.nqg);
+  int64_t nks = (1024 + base - 1) / base;
+  nks = std::min<int64_t>(nks, 8);
+  nks = std::min<int64_t>(nks, std::max(1, (y.nmax + kKeyTile - 1) / kKeyTile));
+  y.nks = (int32_t)std::max<int64_t>(1, nks);
+  y.ncol = std::max(1, (y.nmax + kColKeys - 1) / kColKeys);
+  y.nfuse = std::max(1, (kmax + kFuseRows - 1) / kFuseRows);
+
+  // Plan blob.
+  size_t o = 0;
+  y.p_lp = o; o += sizeof(uint64_t) * LP_COUNT * y.L;
+  y.p_toff = o; o += sizeof(int64_t) * (y.B + 1);
+  y.p_orow = o; o += sizeof(int64_t) * y.L * (y.B + 1);
+  y.p_drow = o; o += sizeof(int64_t) * y.L * (y.B + 1);
+  y.p_nb = o; o += sizeof(int32_t) * y.B;
+  y.p_kk = o; o += sizeof(int32_t) * y.B * y.L;
+  y.p_ns = o; o += sizeof(int32_t) * y.B * y.L;
+  o = (o + 7) & ~size_t(7);
+  y.plan_bytes = o;
+
+  size_t w = 0;
+  y.off_plan = w; w = align_up(w + y.plan_bytes);
+  y.off_qbf = w; w = align_up(w + sizeof(uint16_t) * (size_t)y.Ls * y.B * y.Hq * y.W * y.d);
+  y.off_part = w; w = align_up(w + sizeof(float2) * (size_t)units * y.nks * y.R);
+  y.off_S = w; w = align_up(w + sizeof(float) * (size_t)y.Ls * y.Ntot * y.Hkv);
+  y.off_gs = w; w = align_up(w + (y.mode == VC_RANK_GLOBAL ? sizeof(float) * (size_t)y.Ntot : 0));
+  y.off_drop = w;
+  for (int32_t l = 0; l < y.h; ++l) w = align_up(w + sizeof(int32_t) * (size_t)y.drow[(size_t)l * (y.B + 1) + y.B]);
+  y.total = std::max<size_t>(w, kAlign);
+  return VC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+void viscache_default_params(vc_params *p, double retention) {
+  if (!p) return;
+  p->retention = retention;
+  p->h = 0;
+  p->m = 0.75;
+  p->tau = 1.0f;
+  p->mu = 0.7f;
+  p->rank_mode = VC_RANK_LAYER_HEAD;
+  p->v_out_fp32 = 0;
+}
+
+vc_status viscache_budget(const vc_shape *shape, const vc_params *params, int32_t *k,
+                          int32_t *n_surv, int32_t *h_out) {
+  if (!k || !n_surv) return VC_ERR_ARG;
+  Layout y;
+  vc_status st = make_layout(shape, params, y);
+  if (st != VC_OK) return st;
+  std::memcpy(k, y.k.data(), sizeof(int32_t) * y.k.size());
+  std::memcpy(n_surv, y.ns.data(), sizeof(int32_t) * y.ns.size());
+  if (h_out) *h_out = y.h;
+  return VC_OK;
+}
+
+vc_status viscache_out_rows(const vc_shape *shape, const vc_params *params, int64_t *rows) {
+  if (!rows) return VC_ERR_ARG;
+  Layout y;
+  vc_status st = make_layout(shape, params, y);
+  if (st != VC_OK) return st;
+  std::memcpy(rows, y.orow.data(), sizeof(int64_t) * y.orow.size());
+  return VC_OK;
+}
+
+size_t viscache_prune_workspace_bytes(const vc_shape *shape, const vc_params *params) {
+  Layout y;
+  if (make_layout(shape, params, y) != VC_OK) return 0;
+  return y.total;
+}
+
+vc_status viscache_prune_score_offsets(const vc_shape *shape, const vc_params *params,
+                                       size_t *scores_off, size_t *shared_off) {
+  if (!scores_off || !shared_off) return VC_ERR_ARG;
+  Layout y;
+  vc_status st = make_layout(shape, params, y);
+  if (st != VC_OK) return st;
+  *scores_off = y.off_S;
+  *shared_off = y.mode == VC_RANK_GLOBAL ? y.off_gs : (size_t)-1;
+  return VC_OK;
+}
+
+vc_status viscache_prune(const vc_shape *shape, const vc_params *params, const vc_prune_io *io,
+                         void *workspace, size_t workspace_bytes, void *stream) {
+  return viscache_prune_staged(shape, params, io, workspace, workspace_bytes, stream, nullptr);
+}
+
+vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, const vc_prune_io *io,
+                                void *workspace, size_t workspace_bytes, void *stream,
+                                void *const *events) {
+  Layout y;
+  vc_status st = make_layout(shape, params, y);
+  if (st != VC_OK) return st;
+  if (!io || !io->k_in || !io->v_in || !io->q_win || !io->k_out || !io->v_out || !io->idx_out)
+    return VC_ERR_ARG;
+  if (!workspace || workspace_bytes < y.total) return VC_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return VC_ERR_WORKSPACE;
+  for (int32_t l = 0; l < y.Ls; ++l)
+    if (y.Ntot > 0 && (!io->k_in[l] || !io->q_win[l])) return VC_ERR_ARG;
+  for (int32_t l = 0; l < y.h; ++l) {
+    const int64_t rows = y.orow[(size_t)l * (y.B + 1) + y.B];
+    if (rows > 0 && (!io->v_in[l] || !io->k_out[l] || !io->v_out[l] || !io->idx_out[l]))
+      return VC_ERR_ARG;
+  }
+  if (y.Ntot == 0) return VC_OK;  // nothing to score or keep
+
+  uint8_t *ws = static_cast<uint8_t *>(workspace);
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+
+  // Host copy of the plan.
+  std::vector<uint8_t> blob(y.plan_bytes, 0);
+  auto lp = reinterpret_cast<uint64_t *>(blob.data() + y.p_lp);
+  for (int32_t l = 0; l < y.L; ++l) {
+    lp[LP_K_IN * y.L + l] = reinterpret_cast<uint64_t>(io->k_in[l]);
+    lp[LP_V_IN * y.L + l] = reinterpret_cast<uint64_t>(io->v_in[l]);
+    lp[LP_Q * y.L + l] = reinterpret_cast<uint64_t>(io->q_win[l]);
+    lp[LP_K_OUT * y.L + l] = l < y.h ? reinterpret_cast<uint64_t>(io->k_out[l]) : 0;
+    lp[LP_V_OUT * y.L + l] = l < y.h ? reinterpret_cast<uint64_t>(io->v_out[l]) : 0;
+    lp[LP_IDX * y.L + l] = l < y.h ? reinterpret_cast<uint64_t>(io->idx_out[l]) : 0;
+  }
+  size_t doff = y.off_drop;
+  for (int32_t l = 0; l < y.h; ++l) {
+    const size_t rows = (size_t)y.drow[(size_t)l * (y.B + 1) + y.B];
+    uint64_t dp = reinterpret_cast<uint64_t>(ws + doff);
+    if (io->drop_out && io->drop_out[l]) dp = reinterpret_cast<uint64_t>(io->drop_out[l]);
+    lp[LP_DROP * y.L + l] = dp;
+    doff = align_up(doff + sizeof(int32_t) * rows);
+  }
+  std::memcpy(blob.data() + y.p_toff, y.toff.data(), sizeof(int64_t) * y.toff.size());
+  std::memcpy(blob.data() + y.p_orow, y.orow.data(), sizeof(int64_t) * y.orow.size());
+  std::memcpy(blob.data() + y.p_drow, y.drow.data(), sizeof(int64_t) * y.drow.size());
+  std::memcpy(blob.data() + y.p_nb, y.n.data(), sizeof(int32_t) * y.n.size());
+  std::memcpy(blob.data() + y.p_kk, y.k.data(), sizeof(int32_t) * y.k.size());
+  std::memcpy(blob.data() + y.p_ns, y.ns.data(), sizeof(int32_t) * y.ns.size());
+
+  PrunePlan pl{};
+  pl.B = y.B; pl.L = y.L; pl.Hq = y.Hq; pl.Hkv = y.Hkv; pl.d = y.d; pl.W = y.W; pl.G = y.G;
+  pl.R = y.R; pl.h = y.h; pl.Ls = y.Ls; pl.mode = y.mode; pl.v_fp32 = y.vfp32;
+  pl.nqg = y.nqg; pl.nks = y.nks; pl.ncol = y.ncol; pl.nfuse = y.nfuse; pl.nmax = y.nmax;
+  pl.sc = (float)(1.4426950408889634 / std::sqrt((double)y.d));
+  pl.tc = (float)(1.4426950408889634 / (double)params->tau);
+  pl.mu = params->mu;
+  pl.Ntot = y.Ntot;
+  uint8_t *pb = ws + y.off_plan;
+  pl.lp = reinterpret_cast<const uint64_t *>(pb + y.p_lp);
+  pl.nb = reinterpret_cast<const int32_t *>(pb + y.p_nb);
+  pl.toff = reinterpret_cast<const int64_t *>(pb + y.p_toff);
+  pl.kk = reinterpret_cast<const int32_t *>(pb + y.p_kk);
+  pl.ns = reinterpret_cast<const int32_t *>(pb + y.p_ns);
+  pl.orow = reinterpret_cast<const int64_t *>(pb + y.p_orow);
+  pl.drow = reinterpret_cast<const int64_t *>(pb + y.p_drow);
+  pl.qbf = reinterpret_cast<uint16_t *>(ws + y.off_qbf);
+  pl.part = reinterpret_cast<float2 *>(ws + y.off_part);
+  pl.rowst = nullptr;
+  pl.cnt = nullptr;
+  pl.S = reinterpret_cast<float *>(ws + y.off_S);
+  pl.gs = y.mode == VC_RANK_GLOBAL ? reinterpret_cast<float *>(ws + y.off_gs) : nullptr;
+
+  auto mark = [&](int i) {
+    return events && events[i] ? hipEventRecord(static_cast<hipEvent_t>(events[i]), hs) : hipSuccess;
+  };
+  if (mark(0) != hipSuccess) return VC_ERR_HIP;
+  if (launch_upload(pb, blob.data(), blob.size(), nullptr, 0, hs) != hipSuccess) return VC_ERR_HIP;
+  if (mark(1) != hipSuccess) return VC_ERR_HIP;
+  if (launch_score_stats(pl, hs) != hipSuccess) return VC_ERR_HIP;
+  if (mark(2) != hipSuccess) return VC_ERR_HIP;
+  if (launch_score_colsum(pl, hs) != hipSuccess) return VC_ERR_HIP;
+  if (mark(3) != hipSuccess) return VC_ERR_HIP;
+  if (y.mode == VC_RANK_GLOBAL && launch_score_global(pl, hs) != hipSuccess) return VC_ERR_HIP;
+  if (mark(4) != hipSuccess) return VC_ERR_HIP;
+  if (launch_select(pl, hs) != hipSuccess) return VC_ERR_HIP;
+  if (mark(5) != hipSuccess) return VC_ERR_HIP;
+  if (launch_fuse(pl, hs) != hipSuccess) return VC_ERR_HIP;
+  if (mark(6) != hipSuccess) return VC_ERR_HIP;
+  return VC_OK;
+}
+
+// ---- decode ----------------------------------------------------------------
+
+namespace {
+constexpr int32_t kSplitRows = 512;
+
+vc_status check_decode(const vc_decode_shape *s) {
+  if (!s) return VC_ERR_ARG;
+  if (s->B < 1 || s->L < 1 || s->Hq < 1 || s->Hkv < 1) return VC_ERR_SHAPE;
+  if (s->Hq % s->Hkv != 0) return VC_ERR_SHAPE;
+  if (s->Hq / s->Hkv > 16) return VC_ERR_UNSUPPORTED;
+  if (s->d != 64 && s->d != 128) return VC_ERR_UNSUPPORTED;
+  return VC_OK;
+}
+
+int32_t decode_splits(int64_t max_rows) {
+  return (int32_t)std::max<int64_t>(1, (max_rows + kSplitRows - 1) / kSplitRows);
+}
+}  // namespace
+
+size_t viscache_decode_workspace_bytes(const vc_decode_shape *s, int64_t max_rows) {
+  if (check_decode(s) != VC_OK || max_rows < 0) return 0;
+  const int64_t units = (int64_t)s->L * s->B * s->Hkv;
+  const int64_t ns = decode_splits(max_rows);
+  return align_up(sizeof(float) * (size_t)(units * ns * 16 * s->d)) +
+         align_up(sizeof(float2) * (size_t)(units * ns * 16));
+}
+
+vc_status viscache_append_kv(const vc_decode_shape *s, const vc_cache *c, const void *k_new,
+                             const void *v_new, void *stream) {
+  vc_status st = check_decode(s);
+  if (st != VC_OK) return st;
+  if (!c || !c->k_pool || !c->v_pool || !c->row_off || !c->cap || !c->len || !k_new || !v_new)
+    return VC_ERR_ARG;
+  const int32_t units = s->L * s->B * s->Hkv;
+  if (launch_append(units, s->d, static_cast<uint16_t *>(c->k_pool), static_cast<uint16_t *>(c->v_pool),
+                    c->row_off, c->cap, c->len, static_cast<const uint16_t *>(k_new),
+                    static_cast<const uint16_t *>(v_new), static_cast<hipStream_t>(stream)) != hipSuccess)
+    return VC_ERR_HIP;
+  return VC_OK;
+}
+
+vc_status viscache_decode_attn(const vc_decode_shape *s, const vc_cache *c, const void *q, float *out,
+                               float scale, int64_t max_rows, void *workspace, size_t workspace_bytes,
+                               void *stream) {
+  vc_status st = check_decode(s);
+  if (st != VC_OK) return st;
+  if (!c || !c->k_pool || !c->v_pool || !c->row_off || !c->cap || !c->len || !q || !out) return VC_ERR_ARG;
+  if (!(scale > 0.f) || !std::isfinite(scale) || max_rows < 0) return VC_ERR_ARG;
+  const size_t need = viscache_decode_workspace_bytes(s, max_rows);
+  if (!workspace || workspace_bytes < need) return VC_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return VC_ERR_WORKSPACE;
+  const int64_t units = (int64_t)s->L * s->B * s->Hkv;
+  DecodePlan p{};
+  p.B = s->B; p.L = s->L; p.Hq = s->Hq; p.Hkv = s->Hkv; p.d = s->d; p.G = s->Hq / s->Hkv;
+  p.nsplit = decode_splits(max_rows);
+  p.split_rows = kSplitRows;
+  p.sc = scale * 1.4426950408889634f;
+  p.k_pool = static_cast<const uint16_t *>(c->k_pool);
+  p.v_pool = static_cast<const uint16_t *>(c->v_pool);
+  p.row_off = c->row_off;
+  p.cap = c->cap;
+  p.len = c->len;
+  p.q = static_cast<const uint16_t *>(q);
+  p.out = out;
+  uint8_t *ws = static_cast<uint8_t *>(workspace);
+  p.part_o = reinterpret_cast<float *>(ws);
+  p.part_ml = reinterpret_cast<float2 *>(ws + align_up(sizeof(float) * (size_t)(units * p.nsplit * 16 * s->d)));
+  if (launch_decode(p, static_cast<hipStream_t>(stream)) != hipSuccess) return VC_ERR_HIP;
+  return VC_OK;
+}
+
+const char *viscache_strerror(vc_status s) {
+  switch (s) {
+    case VC_OK: return "ok";
+    case VC_ERR_ARG: return "invalid argument";
+    case VC_ERR_SHAPE: return "invalid shape";
+    case VC_ERR_BUDGET: return "no valid budget for these retention parameters";
+    case VC_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case VC_ERR_UNSUPPORTED: return "shape not supported by the kernels";
+    case VC_ERR_HIP: return "HIP launch failed";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

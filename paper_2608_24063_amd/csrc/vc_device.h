@@ -1,0 +1,63 @@
+// vc_device.h -- gfx950 device helpers for the PruneKV kernels: bf16 vector
+// types, the 16x16x32 bf16 MFMA, wave64 shuffles and the XCD-aware block
+// remap.  Internal to libviscache.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace vc {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kXcds = 8;  // MI355X: 8 accelerator complex dies, 32 CUs each
+
+// D = A(16x32) * B(32x16) + C on the matrix cores.  Lane l holds row l%16 of A
+// and column l%16 of B, each with the 8 k-elements of lane group l/16; D comes
+// back with column l%16 and rows 4*(l/16)+i in element i.  Callers pick the
+// same k-element order for A and B, so the order itself is free.
+__device__ __forceinline__ f32x4 mfma_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ u32x4 as_u32x4(bf16x8 v) { return __builtin_bit_cast(u32x4, v); }
+
+// Two fp32 -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  bf16x2 v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Round a float to bf16 precision and return it as float.
+__device__ __forceinline__ float round_bf16(float x) {
+  return __uint_as_float(pack_bf16(x, 0.f) << 16);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+template <typename T>
+__device__ __forceinline__ T shfl_xor(T v, int mask) {
+  return __shfl_xor(v, mask, 64);
+}
+
+// Block index remapped so that consecutive logical indices land on the same
+// XCD: the hardware deals workgroups round-robin over the 8 XCDs, and each XCD
+// has its own L2.  Logical blocks [x*per, (x+1)*per) run on XCD x.
+__device__ __forceinline__ uint32_t xcd_block(uint32_t bid, uint32_t nblocks) {
+  uint32_t per = nblocks / kXcds, rem = nblocks % kXcds;
+  uint32_t x = bid % kXcds, slot = bid / kXcds;
+  // XCDs [0, rem) receive per+1 blocks, the others per.
+  uint32_t base = x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per;
+  return base + slot;
+}
+
+}  // namespace vc

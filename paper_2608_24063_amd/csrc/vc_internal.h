@@ -1,0 +1,83 @@
+// vc_internal.h -- plan passed by value to the PruneKV kernels, and the host
+// launchers each kernel file exports to the C ABI layer.  Internal.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace vc {
+
+// Indices into the per-layer pointer table.
+enum { LP_K_IN = 0, LP_V_IN, LP_Q, LP_K_OUT, LP_V_OUT, LP_IDX, LP_DROP, LP_COUNT };
+
+// Tile sizes shared by host-side grid sizing and the kernels.
+constexpr int kStatsRows = 256;   // query rows per stats workgroup (4 waves x 64)
+constexpr int kKeyTile = 64;      // keys staged per LDS tile
+constexpr int kColKeys = 256;     // keys per column-sum workgroup (4 waves x 64)
+constexpr int kFuseRows = 64;     // kept rows per fusion workgroup (4 waves x 16)
+constexpr int kDropTile = 64;     // dropped rows staged per LDS tile
+constexpr int kSelectThreads = 1024;
+constexpr int kSelectPerThread = 32;  // => n <= 32768 tokens per sequence
+constexpr int kMaxTokens = kSelectThreads * kSelectPerThread;
+
+// Everything the prune kernels need, by value (a few hundred bytes).  Array
+// members point into the device workspace, filled by the plan upload kernel.
+struct PrunePlan {
+  int32_t B, L, Hq, Hkv, d, W, G, R;
+  int32_t h;          // truncation layer: layers [0, h) keep tokens
+  int32_t Ls;         // scored layers: h (layer/head ranking) or L (global)
+  int32_t mode;       // 0 layer/head, 1 global
+  int32_t v_fp32;     // fused values stored as fp32
+  int32_t nqg, nks;   // stats grid: query groups x key splits per unit
+  int32_t ncol;       // column-sum chunks per unit (max over sequences)
+  int32_t nfuse;      // fusion tiles per unit (max over units)
+  int32_t nmax;       // max n_b
+  float sc;           // log2(e) / sqrt(d)
+  float tc;           // log2(e) / tau
+  float mu;
+  int64_t Ntot;       // sum_b n_b
+  const uint64_t *lp;   // [LP_COUNT][L] per-layer device pointers
+  const int32_t *nb;    // [B]
+  const int64_t *toff;  // [B+1] token offsets
+  const int32_t *kk;    // [B*L] kept per (b, l)
+  const int32_t *ns;    // [B*L] survivors per (b, l)
+  const int64_t *orow;  // [L*(B+1)] output row offsets per layer
+  const int64_t *drow;  // [L*(B+1)] dropped-row offsets per layer
+  uint16_t *qbf;        // [Ls][B][Hq][W][d] window queries in bf16
+  float2 *part;         // [U][nks][R] partial row statistics (max*sc, sum)
+  float2 *rowst;        // [U][R] row statistics (max*sc, 1/sum)
+  uint32_t *cnt;        // [U] arrival counters of the stats kernel
+  float *S;             // [Ls][Ntot*Hkv] window scores
+  float *gs;            // [Ntot] shared (global) scores
+};
+
+// Host-side launchers (each returns hipSuccess or the launch error).
+hipError_t launch_upload(uint8_t *dst, const uint8_t *src, size_t bytes, uint32_t *zero,
+                         size_t zero_words, hipStream_t st);
+hipError_t launch_score_stats(const PrunePlan &p, hipStream_t st);
+hipError_t launch_score_colsum(const PrunePlan &p, hipStream_t st);
+hipError_t launch_score_global(const PrunePlan &p, hipStream_t st);
+hipError_t launch_select(const PrunePlan &p, hipStream_t st);
+hipError_t launch_fuse(const PrunePlan &p, hipStream_t st);
+
+struct DecodePlan {
+  int32_t B, L, Hq, Hkv, d, G;
+  int32_t nsplit;    // row splits per unit
+  int32_t split_rows;
+  float sc;          // scale * log2(e)
+  const uint16_t *k_pool, *v_pool;
+  const int64_t *row_off;
+  const int32_t *cap;
+  const int32_t *len;
+  const uint16_t *q;
+  float *out;
+  float *part_o;     // [U][nsplit][16][d]
+  float2 *part_ml;   // [U][nsplit][16]
+};
+
+hipError_t launch_append(int32_t units, int32_t d, uint16_t *k_pool, uint16_t *v_pool,
+                         const int64_t *row_off, const int32_t *cap, int32_t *len,
+                         const uint16_t *k_new, const uint16_t *v_new, hipStream_t st);
+hipError_t launch_decode(const DecodePlan &p, hipStream_t st);
+
+}  // namespace vc

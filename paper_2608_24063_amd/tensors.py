@@ -1,0 +1,119 @@
+"""PyTorch-side marshalling for libviscache: allocates the outputs and the
+workspace that the C ABI asks for and passes device addresses and the current
+stream.  No computation happens here."""
+from __future__ import annotations
+
+import torch
+
+from . import (VC_PRUNE_EVENTS, VC_RANK_GLOBAL, make_params, make_shape, vc_cache, vc_decode_shape,
+               viscache_append_kv, viscache_budget, viscache_decode_attn, viscache_decode_workspace_bytes,
+               viscache_out_rows, viscache_prune, viscache_prune_staged, viscache_prune_workspace_bytes)
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _addr(t: torch.Tensor | None) -> int:
+    return 0 if t is None or t.numel() == 0 else t.data_ptr()
+
+
+class PruneCall:
+    """One PruneKV problem: shape, parameters, per-layer outputs, workspace.
+
+    k_in / v_in: per-layer bf16 tensors [sum_b Hkv*n_b, d]; q_win: per-layer
+    fp32 tensors [B, Hq, W, d].  `run()` enqueues viscache_prune on the
+    current stream."""
+
+    def __init__(self, B, L, Hq, Hkv, d, W, n_vis, params, k_in, v_in, q_win, with_drop=False):
+        self.B, self.L, self.Hq, self.Hkv, self.d, self.W = B, L, Hq, Hkv, d, W
+        self.n_vis = [int(x) for x in n_vis]
+        self.params = params
+        self.shape = make_shape(B, L, Hq, Hkv, d, W, self.n_vis)
+        self.k, self.n_surv, self.h = viscache_budget(self.shape, params)
+        self.rows = viscache_out_rows(self.shape, params)
+        dev = k_in[0].device
+        vdt = torch.float32 if params.v_out_fp32 else torch.bfloat16
+        self.k_in, self.v_in, self.q_win = list(k_in), list(v_in), list(q_win)
+        self.k_out, self.v_out, self.idx_out, self.drop_out = [], [], [], []
+        for l in range(L):
+            nrow = self.rows[l * (B + 1) + B]
+            self.k_out.append(torch.empty((nrow, d), dtype=torch.bfloat16, device=dev))
+            self.v_out.append(torch.empty((nrow, d), dtype=vdt, device=dev))
+            self.idx_out.append(torch.empty((nrow,), dtype=torch.int32, device=dev))
+            if with_drop:
+                ndrop = sum(Hkv * (self.n_surv[b * L + l] - self.k[b * L + l]) for b in range(B)) if l < self.h else 0
+                self.drop_out.append(torch.empty((ndrop,), dtype=torch.int32, device=dev))
+        self.ws_bytes = viscache_prune_workspace_bytes(self.shape, params)
+        self.ws = torch.empty((self.ws_bytes,), dtype=torch.uint8, device=dev)
+
+    @property
+    def global_rank(self) -> bool:
+        return self.params.rank_mode == VC_RANK_GLOBAL
+
+    def _args(self):
+        return (self.shape, self.params,
+                [_addr(t) for t in self.k_in], [_addr(t) for t in self.v_in],
+                [_addr(t) for t in self.q_win], [_addr(t) for t in self.k_out],
+                [_addr(t) for t in self.v_out], [_addr(t) for t in self.idx_out],
+                self.ws.data_ptr(), self.ws_bytes, _stream())
+
+    def run(self, events=None) -> None:
+        """Enqueue viscache_prune; with `events` (VC_PRUNE_EVENTS torch.cuda.Event
+        objects created with enable_timing=True) the stages are bracketed."""
+        drop = [_addr(t) for t in self.drop_out] if self.drop_out else None
+        if events is None:
+            viscache_prune(*self._args(), drop_out=drop)
+        else:
+            assert len(events) == VC_PRUNE_EVENTS
+            for e in events:
+                if e.cuda_event == 0:
+                    e.record()  # materialise the handle
+            viscache_prune_staged(*self._args(), [e.cuda_event for e in events], drop_out=drop)
+
+    def unit_rows(self, l: int, b: int, g: int):
+        """Row range of (layer, sequence, kv head) in layer l's outputs."""
+        k = self.k[b * self.L + l]
+        r0 = self.rows[l * (self.B + 1) + b] + g * k
+        return r0, r0 + k
+
+    def unit_drop_rows(self, l: int, b: int, g: int):
+        r = self.n_surv[b * self.L + l] - self.k[b * self.L + l]
+        base = sum(self.Hkv * (self.n_surv[bb * self.L + l] - self.k[bb * self.L + l]) for bb in range(b))
+        return base + g * r, base + (g + 1) * r
+
+
+class DecodeCache:
+    """A decode cache pool over L layers x B sequences x Hkv heads.  Unit
+    u = (l*B + b)*Hkv + g owns `cap[u]` rows starting at row_off[u]."""
+
+    def __init__(self, L, B, Hq, Hkv, d, caps, device):
+        self.shape = vc_decode_shape(B, L, Hq, Hkv, d)
+        self.L, self.B, self.Hq, self.Hkv, self.d = L, B, Hq, Hkv, d
+        caps = [int(c) for c in caps]
+        offs, o = [], 0
+        for c in caps:
+            offs.append(o)
+            o += c
+        self.total_rows = o
+        self.max_cap = max(caps) if caps else 0
+        self.k_pool = torch.zeros((max(o, 1), d), dtype=torch.bfloat16, device=device)
+        self.v_pool = torch.zeros((max(o, 1), d), dtype=torch.bfloat16, device=device)
+        self.row_off = torch.tensor(offs, dtype=torch.int64, device=device)
+        self.cap = torch.tensor(caps, dtype=torch.int32, device=device)
+        self.len = torch.zeros(len(caps), dtype=torch.int32, device=device)
+        self.offs_host, self.caps_host = offs, caps
+        self.ws_bytes = viscache_decode_workspace_bytes(self.shape, self.max_cap)
+        self.ws = torch.empty((max(self.ws_bytes, 256),), dtype=torch.uint8, device=device)
+        self.c = vc_cache(self.k_pool.data_ptr(), self.v_pool.data_ptr(), self.row_off.data_ptr(),
+                          self.cap.data_ptr(), self.len.data_ptr())
+
+    def append(self, k_new: torch.Tensor, v_new: torch.Tensor) -> None:
+        viscache_append_kv(self.shape, self.c, k_new.data_ptr(), v_new.data_ptr(), _stream())
+
+    def attend(self, q: torch.Tensor, out: torch.Tensor, scale: float) -> None:
+        viscache_decode_attn(self.shape, self.c, q.data_ptr(), out.data_ptr(), scale, self.max_cap,
+                             self.ws.data_ptr(), self.ws_bytes, _stream())
+
+
+__all__ = ["PruneCall", "DecodeCache", "make_params"]

@@ -1,0 +1,150 @@
+"""GPU parity of viscache_append_kv / viscache_decode_attn against the oracle's
+decode attention (Sec. 2, decoding), through the C ABI, including decode over
+a cache that viscache_prune has just compressed."""
+import numpy as np
+import pytest
+
+from tests.parity import fused_error
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+TOL = 1e-4
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2608_24063_amd as vc
+    vc.lib()
+    return torch.device("cuda:0")
+
+
+def _bits(sg, seed, stream, shape):
+    return sg.normal_bf16(seed, stream, shape)
+
+
+def _check_out(orc, q, K, V, out, scale, what):
+    ref = orc.attend(q, K, V, scale)
+    err = fused_error(ref[None, :], out[None, :])
+    assert err <= TOL, f"{what}: decode error {err}"
+
+
+@pytest.mark.parametrize("d,Hq,Hkv", [(128, 8, 2), (64, 28, 4), (128, 64, 8)])
+def test_decode_random_caches(dev, orc, sg, d, Hq, Hkv):
+    from paper_2608_24063_amd.tensors import DecodeCache
+    from synthgen.device import bf16_tensor, to_host_bf16
+    L, B = 2, 2
+    units = L * B * Hkv
+    lens = [0, 1, 31, 33, 100, 511, 512, 513, 1100, 5, 64, 700, 2, 1025, 47, 256][:units]
+    lens += [17] * (units - len(lens))
+    caps = [x + 3 for x in lens]
+    c = DecodeCache(L, B, Hq, Hkv, d, caps, dev)
+    Kp = _bits(sg, 7, 1, (c.total_rows, d))
+    Vp = _bits(sg, 7, 2, (c.total_rows, d))
+    c.k_pool.copy_(bf16_tensor(Kp, dev))
+    c.v_pool.copy_(bf16_tensor(Vp, dev))
+    c.len.copy_(torch.tensor(lens, dtype=torch.int32))
+    q = _bits(sg, 7, 3, (L, B, Hq, d))
+    out = torch.full((L, B, Hq, d), float("nan"), dtype=torch.float32, device=dev)
+    scale = d ** -0.5
+    c.attend(bf16_tensor(q, dev), out, scale)
+    torch.cuda.synchronize()
+    o = out.cpu().numpy()
+    G = Hq // Hkv
+    for l in range(L):
+        for b in range(B):
+            for g in range(Hkv):
+                u = (l * B + b) * Hkv + g
+                r0, n = c.offs_host[u], lens[u]
+                for hh in range(G):
+                    h = g * G + hh
+                    if n == 0:
+                        assert np.all(o[l, b, h] == 0)
+                        continue
+                    _check_out(orc, q[l, b, h], Kp[r0:r0 + n], Vp[r0:r0 + n], o[l, b, h], scale,
+                               f"l={l} b={b} h={h} n={n}")
+
+
+def test_append_respects_capacity(dev, sg):
+    from paper_2608_24063_amd.tensors import DecodeCache
+    from synthgen.device import bf16_tensor, to_host_bf16
+    L, B, Hq, Hkv, d = 2, 1, 4, 2, 64
+    caps = [3, 2, 5, 1]
+    c = DecodeCache(L, B, Hq, Hkv, d, caps, dev)
+    c.len.copy_(torch.tensor([0, 2, 4, 0], dtype=torch.int32))
+    kn = _bits(sg, 9, 1, (L, B, Hkv, d))
+    vn = _bits(sg, 9, 2, (L, B, Hkv, d))
+    c.append(bf16_tensor(kn, dev), bf16_tensor(vn, dev))
+    torch.cuda.synchronize()
+    assert c.len.cpu().tolist() == [1, 2, 5, 1]
+    K = to_host_bf16(c.k_pool)
+    V = to_host_bf16(c.v_pool)
+    kn2, vn2 = kn.reshape(-1, d), vn.reshape(-1, d)
+    for u, pos in [(0, 0), (2, 4), (3, 0)]:
+        np.testing.assert_array_equal(K[c.offs_host[u] + pos], kn2[u])
+        np.testing.assert_array_equal(V[c.offs_host[u] + pos], vn2[u])
+    assert np.all(K[c.offs_host[1]:c.offs_host[1] + 2] == 0)  # full unit untouched
+
+
+def test_decode_over_pruned_cache(dev, orc, sg):
+    """prune -> cache of (kept visual | text window | generated) rows ->
+    append + attend for a few steps, each step checked against the oracle."""
+    import paper_2608_24063_amd as vc
+    from paper_2608_24063_amd.tensors import DecodeCache, PruneCall
+    from synthgen.device import bf16_tensor, to_host_bf16, upload_layers
+    w = sg.TINY
+    n = [int(x) for x in w.n_vis()]
+    params = vc.make_params(w.retention)
+    dv, host = upload_layers(w, range(w.L), dev, keep_host=True)
+    pc = PruneCall(w.B, w.L, w.Hq, w.Hkv, w.d, w.W, n, params, [dv["K"][l] for l in range(w.L)],
+                   [dv["V"][l] for l in range(w.L)], [dv["Q"][l] for l in range(w.L)])
+    pc.run()
+    steps = 6
+    caps, kept_rows = [], []
+    for l in range(w.L):
+        for b in range(w.B):
+            for g in range(w.Hkv):
+                k = pc.k[b * w.L + l]
+                kept_rows.append(k)
+                caps.append(k + w.W + steps)
+    c = DecodeCache(w.L, w.B, w.Hq, w.Hkv, w.d, caps, dev)
+    text_k = _bits(sg, w.seed, 11, (len(caps), w.W, w.d))
+    text_v = _bits(sg, w.seed, 12, (len(caps), w.W, w.d))
+    lens = []
+    for l in range(w.L):
+        for b in range(w.B):
+            for g in range(w.Hkv):
+                u = (l * w.B + b) * w.Hkv + g
+                r0 = c.offs_host[u]
+                k = kept_rows[u]
+                if k:
+                    a0, a1 = pc.unit_rows(l, b, g)
+                    c.k_pool[r0:r0 + k] = pc.k_out[l][a0:a1]
+                    c.v_pool[r0:r0 + k] = pc.v_out[l][a0:a1]
+                c.k_pool[r0 + k:r0 + k + w.W] = bf16_tensor(text_k[u], dev)
+                c.v_pool[r0 + k:r0 + k + w.W] = bf16_tensor(text_v[u], dev)
+                lens.append(k + w.W)
+    c.len.copy_(torch.tensor(lens, dtype=torch.int32))
+    scale = w.d ** -0.5
+    out = torch.empty((w.L, w.B, w.Hq, w.d), dtype=torch.float32, device=dev)
+    for t in range(steps):
+        kn = _bits(sg, w.seed, 100 + 3 * t, (w.L, w.B, w.Hkv, w.d))
+        vn = _bits(sg, w.seed, 101 + 3 * t, (w.L, w.B, w.Hkv, w.d))
+        q = _bits(sg, w.seed, 102 + 3 * t, (w.L, w.B, w.Hq, w.d))
+        c.append(bf16_tensor(kn, dev), bf16_tensor(vn, dev))
+        c.attend(bf16_tensor(q, dev), out, scale)
+        torch.cuda.synchronize()
+        K, V, o = to_host_bf16(c.k_pool), to_host_bf16(c.v_pool), out.cpu().numpy()
+        ln = c.len.cpu().numpy()
+        for l in range(w.L):
+            for b in range(w.B):
+                for g in range(w.Hkv):
+                    u = (l * w.B + b) * w.Hkv + g
+                    assert ln[u] == lens[u] + t + 1
+                    r0 = c.offs_host[u]
+                    for hh in (0, w.G - 1):
+                        h = g * w.G + hh
+                        _check_out(orc, q[l, b, h], K[r0:r0 + ln[u]], V[r0:r0 + ln[u]], o[l, b, h], scale,
+                                   f"step {t} l={l} h={h}")

@@ -1,0 +1,373 @@
+"""GPU parity of viscache_prune against the oracle, through the C ABI.
+
+Small workloads are compared unit by unit in full; the full-size workloads run
+in the benchmark's launch configuration and are compared on sampled units
+(each unit is independent in the layer/head ranking) plus properties that hold
+at any size."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from tests.parity import TOL_BF16, TOL_FP32, check_sets, fused_error, rel_err
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2608_24063_amd as vc
+    vc.lib()
+    return torch.device("cuda:0")
+
+
+def _diag(rec):
+    d = os.environ.get("VC_DIAG_DIR")
+    if d:
+        os.makedirs(d, exist_ok=True)
+        with open(os.path.join(d, "parity_diag.jsonl"), "a") as f:
+            f.write(json.dumps(rec) + "\n")
+
+
+class Run:
+    """One viscache_prune call on a seeded workload, with host copies."""
+
+    def __init__(self, w, dev, mode=0, vfp32=False, rr=None, h=0, m=0.75, tau=1.0, mu=0.7):
+        import paper_2608_24063_amd as vc
+        from paper_2608_24063_amd.tensors import PruneCall
+        from synthgen.device import to_host_bf16, upload_layers
+        self.w, self.mode, self.vfp32, self.tau, self.mu = w, mode, vfp32, tau, mu
+        self.params = vc.make_params(rr if rr is not None else w.retention, h=h, m=m, tau=tau, mu=mu,
+                                     rank_mode=mode, v_out_fp32=vfp32)
+        self.n = [int(x) for x in w.n_vis()]
+        self.toff = np.concatenate([[0], np.cumsum(self.n)]).astype(np.int64)
+        shape = vc.make_shape(w.B, w.L, w.Hq, w.Hkv, w.d, w.W, self.n)
+        _, _, self.h = vc.viscache_budget(shape, self.params)
+        self.Ls = w.L if mode == vc.VC_RANK_GLOBAL else self.h
+        dev_t, self.host = upload_layers(w, range(self.Ls), dev, keep_host=True)
+        pc = PruneCall(w.B, w.L, w.Hq, w.Hkv, w.d, w.W, self.n, self.params,
+                       [dev_t["K"].get(l) for l in range(w.L)], [dev_t["V"].get(l) for l in range(w.L)],
+                       [dev_t["Q"].get(l) for l in range(w.L)], with_drop=True)
+        pc.run()
+        torch.cuda.synchronize()
+        self.pc = pc
+        self.k, self.ns = pc.k, pc.n_surv
+        self.idx = [t.cpu().numpy() for t in pc.idx_out]
+        self.drop = [t.cpu().numpy() for t in pc.drop_out]
+        self.kout = [to_host_bf16(t) for t in pc.k_out]
+        self.vout = [t.float().cpu().numpy() for t in pc.v_out]
+        s_off, g_off = vc.viscache_prune_score_offsets(shape, self.params)
+        ntot = int(self.toff[-1])
+        nS = self.Ls * ntot * w.Hkv
+        self.S = pc.ws[s_off:s_off + 4 * nS].view(torch.float32).cpu().numpy().reshape(self.Ls, -1)
+        self.gs = pc.ws[g_off:g_off + 4 * ntot].view(torch.float32).cpu().numpy() if g_off is not None else None
+        del dev_t
+
+    # host views of one unit
+    def unit_kv(self, role, l, b, g):
+        n = self.n[b]
+        r0 = int(self.toff[b]) * self.w.Hkv + g * n
+        return self.host[role][l][r0:r0 + n]
+
+    def unit_q(self, l, b, g):
+        G = self.w.G
+        return self.host["Q"][l][b, g * G:(g + 1) * G].reshape(-1, self.w.d)
+
+    def gpu_scores(self, l, b, g):
+        n = self.n[b]
+        r0 = int(self.toff[b]) * self.w.Hkv + g * n
+        return self.S[l][r0:r0 + n]
+
+    def gpu_unit(self, l, b, g):
+        r0, r1 = self.pc.unit_rows(l, b, g)
+        d0, d1 = self.pc.unit_drop_rows(l, b, g)
+        return self.idx[l][r0:r1], self.drop[l][d0:d1], self.kout[l][r0:r1], self.vout[l][r0:r1]
+
+    def check_unit(self, orc, l, b, g, S32=None):
+        """Full comparison of one unit; S32 = the oracle's ranking scores
+        (computed here for the layer/head ranking)."""
+        K, V = self.unit_kv("K", l, b, g), self.unit_kv("V", l, b, g)
+        k, ns = self.k[b * self.w.L + l], self.ns[b * self.w.L + l]
+        if S32 is None:
+            S32 = orc.scores_unit(K, self.unit_q(l, b, g)).astype(np.float32)
+        kept, drop, krows, vrows = self.gpu_unit(l, b, g)
+        swaps = check_sets(S32, k, ns, kept, drop, what=f"{self.w.name} l={l} b={b} g={g}")
+        np.testing.assert_array_equal(krows, K[kept])  # kept keys are bit copies
+        ref = orc.fuse(V, kept.astype(np.int32), drop.astype(np.int32), self.tau, self.mu)
+        ferr = fused_error(ref, vrows)
+        tol = TOL_FP32 if self.vfp32 else TOL_BF16
+        assert ferr <= tol, f"fused V error {ferr} > {tol} at l={l} b={b} g={g}"
+        return swaps, ferr
+
+    def check_all_layer_head(self, orc, units):
+        def one(u):
+            l, b, g = u
+            S32 = orc.scores_unit(self.unit_kv("K", l, b, g), self.unit_q(l, b, g)).astype(np.float32)
+            return S32
+        refs = orc.run_units(one, units)
+        swaps, ferr, serr = 0, 0.0, 0.0
+        for (l, b, g), S32 in zip(units, refs):
+            s, f = self.check_unit(orc, l, b, g, S32)
+            swaps += s
+            ferr = max(ferr, f)
+            serr = max(serr, rel_err(S32, self.gpu_scores(l, b, g), floor=1e-30))
+        _diag(dict(workload=self.w.name, mode=self.mode, vfp32=self.vfp32, units=len(units),
+                   swaps=swaps, fused_err=ferr, score_rel_err=serr))
+        return swaps, ferr, serr
+
+
+def _all_units(r):
+    return [(l, b, g) for l in range(r.h) for b in range(r.w.B) for g in range(r.w.Hkv)]
+
+
+# ---------------------------------------------------------------- tiny, full
+@pytest.mark.parametrize("vfp32", [False, True])
+def test_tiny_layer_head_full(dev, orc, sg, vfp32):
+    r = Run(sg.TINY, dev, vfp32=vfp32)
+    swaps, ferr, serr = r.check_all_layer_head(orc, _all_units(r))
+    assert serr < 1e-4
+
+
+@pytest.mark.parametrize("vfp32", [False, True])
+def test_tiny_global_full(dev, orc, sg, vfp32):
+    r = Run(sg.TINY, dev, mode=1, vfp32=vfp32)
+    w = r.w
+    for b in range(w.B):
+        units = [(l, b, g) for l in range(w.L) for g in range(w.Hkv)]
+        S = orc.run_units(lambda u: orc.scores_unit(r.unit_kv("K", *u), r.unit_q(*u)), units)
+        s32 = orc.global_scores(S)
+        n = r.n[b]
+        gs = r.gs[r.toff[b]:r.toff[b] + n]
+        assert rel_err(s32, gs, floor=1e-30) < 1e-4
+        for l in range(r.h):
+            for g in range(w.Hkv):
+                r.check_unit(orc, l, b, g, S32=s32)
+        # one shared ranking: deeper layers keep subsets of shallower ones
+        for l in range(1, r.h):
+            k0, _, _, _ = r.gpu_unit(l - 1, b, 0)
+            k1, _, _, _ = r.gpu_unit(l, b, 0)
+            assert set(k1.tolist()) <= set(k0.tolist())
+
+
+# ------------------------------------------------------------ edge cases
+def _custom(sg, **kw):
+    base = dict(name="edge", seed=0x5EED00E1, B=1, L=4, Hq=8, Hkv=2, d=64, W=32, tokens_per_frame=64,
+                frames=8, retention=0.25)
+    base.update(kw)
+    return sg.Workload(**base)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_ragged_small_batch(dev, orc, sg, d):
+    # jittered frame counts with tiny frames give ragged sequences, one of
+    # them below a tile; G = 3 and W = 5 make ragged query rows.
+    w = _custom(sg, B=5, Hq=6, Hkv=2, d=d, W=5, tokens_per_frame=7, frames=12, frame_jitter=11)
+    for vfp32 in (False, True):
+        r = Run(w, dev, vfp32=vfp32)
+        r.check_all_layer_head(orc, _all_units(r))
+
+
+def test_empty_sequence_in_batch(dev, orc, sg):
+    import paper_2608_24063_amd as vc
+    from paper_2608_24063_amd.tensors import PruneCall
+    from synthgen.device import bf16_tensor
+    w = _custom(sg, B=1)
+    n = [0, 130, 0, 64]
+    rng = np.random.default_rng(0)
+    rows = sum(n) * w.Hkv
+    K = [rng.integers(0, 2 ** 15, (rows, w.d), dtype=np.uint16) & 0x3FFF for _ in range(w.L)]
+    V = [rng.integers(0, 2 ** 15, (rows, w.d), dtype=np.uint16) & 0x3FFF for _ in range(w.L)]
+    Q = [rng.standard_normal((4, w.Hq, w.W, w.d)).astype(np.float32) for _ in range(w.L)]
+    params = vc.make_params(0.25)
+    pc = PruneCall(4, w.L, w.Hq, w.Hkv, w.d, w.W, n, params, [bf16_tensor(x, dev) for x in K],
+                   [bf16_tensor(x, dev) for x in V], [torch.from_numpy(q).to(dev) for q in Q], with_drop=True)
+    pc.run()
+    torch.cuda.synchronize()
+    toff = np.concatenate([[0], np.cumsum(n)])
+    for l in range(pc.h):
+        for b in range(4):
+            for g in range(w.Hkv):
+                nb = n[b]
+                r0 = toff[b] * w.Hkv + g * nb
+                Ku, Vu = K[l][r0:r0 + nb], V[l][r0:r0 + nb]
+                Qu = Q[l][b, g * w.G:(g + 1) * w.G].reshape(-1, w.d)
+                k, ns = pc.k[b * w.L + l], pc.n_surv[b * w.L + l]
+                a0, a1 = pc.unit_rows(l, b, g)
+                d0, d1 = pc.unit_drop_rows(l, b, g)
+                kept = pc.idx_out[l][a0:a1].cpu().numpy()
+                drop = pc.drop_out[l][d0:d1].cpu().numpy()
+                if nb == 0:
+                    assert k == 0 and len(kept) == 0
+                    continue
+                S32 = orc.scores_unit(Ku, Qu).astype(np.float32)
+                check_sets(S32, k, ns, kept, drop)
+                ref = orc.fuse(Vu, kept.astype(np.int32), drop.astype(np.int32))
+                got = pc.v_out[l][a0:a1].float().cpu().numpy()
+                assert fused_error(ref, got) <= TOL_BF16
+
+
+def test_keep_all_returns_cache_unchanged(dev, orc, sg):
+    # RR = 1, h = L, m = 1: every layer keeps every token, nothing is fused.
+    w = _custom(sg, L=3)
+    for vfp32 in (False, True):
+        r = Run(w, dev, rr=1.0, h=3, m=1.0, vfp32=vfp32)
+        for l in range(w.L):
+            for g in range(w.Hkv):
+                kept, drop, krows, vrows = r.gpu_unit(l, 0, g)
+                n = r.n[0]
+                np.testing.assert_array_equal(kept, np.arange(n))
+                assert len(drop) == 0
+                np.testing.assert_array_equal(krows, r.unit_kv("K", l, 0, g))
+                V = r.unit_kv("V", l, 0, g)
+                np.testing.assert_array_equal(vrows, sg.bf16_bits_to_f32(V))
+
+
+def test_mu_one_is_plain_pruning(dev, orc, sg):
+    w = _custom(sg)
+    r = Run(w, dev, mu=1.0, vfp32=True)
+    for (l, b, g) in _all_units(r):
+        kept, drop, krows, vrows = r.gpu_unit(l, b, g)
+        np.testing.assert_array_equal(vrows, sg.bf16_bits_to_f32(r.unit_kv("V", l, b, g)[kept]))
+
+
+@pytest.mark.parametrize("tau", [0.05, 50.0])
+def test_temperature(dev, orc, sg, tau):
+    w = _custom(sg, seed=0x5EED00E2)
+    r = Run(w, dev, tau=tau, vfp32=True)
+    r.check_all_layer_head(orc, _all_units(r))
+
+
+def test_identical_keys_tie_to_lowest_index(dev, orc, sg):
+    import paper_2608_24063_amd as vc
+    from paper_2608_24063_amd.tensors import PruneCall
+    from synthgen.device import bf16_tensor
+    L, Hq, Hkv, d, W, n = 4, 8, 2, 64, 8, 300
+    rng = np.random.default_rng(1)
+    row = rng.integers(0, 2 ** 14, (1, d), dtype=np.uint16)
+    K = [np.repeat(row, Hkv * n, 0) for _ in range(L)]
+    V = [rng.integers(0, 2 ** 14, (Hkv * n, d), dtype=np.uint16) for _ in range(L)]
+    Q = [rng.standard_normal((1, Hq, W, d)).astype(np.float32) for _ in range(L)]
+    params = vc.make_params(0.25)
+    pc = PruneCall(1, L, Hq, Hkv, d, W, [n], params, [bf16_tensor(x, dev) for x in K],
+                   [bf16_tensor(x, dev) for x in V], [torch.from_numpy(q).to(dev) for q in Q], with_drop=True)
+    pc.run()
+    torch.cuda.synchronize()
+    for l in range(pc.h):
+        for g in range(Hkv):
+            a0, a1 = pc.unit_rows(l, 0, g)
+            d0, d1 = pc.unit_drop_rows(l, 0, g)
+            k, ns = pc.k[l], pc.n_surv[l]
+            np.testing.assert_array_equal(pc.idx_out[l][a0:a1].cpu().numpy(), np.arange(k))
+            np.testing.assert_array_equal(pc.drop_out[l][d0:d1].cpu().numpy(), np.arange(k, ns))
+
+
+def test_repeat_is_bitwise_deterministic(dev, sg):
+    w = _custom(sg)
+    a = Run(w, dev)
+    b = Run(w, dev)
+    for l in range(a.h):
+        np.testing.assert_array_equal(a.idx[l], b.idx[l])
+        np.testing.assert_array_equal(a.vout[l], b.vout[l])
+    np.testing.assert_array_equal(a.S, b.S)
+
+
+# ----------------------------------------------------------- 7B-shaped, full
+@pytest.fixture(scope="module")
+def run7b(dev, sg):
+    return Run(sg.VLLM7B, dev)
+
+
+def test_vllm7b_layer_head_full(run7b, orc):
+    swaps, ferr, serr = run7b.check_all_layer_head(orc, _all_units(run7b))
+    assert serr < 1e-4
+
+
+def test_vllm7b_fp32_out(dev, orc, sg):
+    r = Run(sg.VLLM7B, dev, vfp32=True)
+    units = [(0, 0, 0), (10, 0, 1), (r.h - 1, 0, 3)]
+    r.check_all_layer_head(orc, units)
+
+
+def test_vllm7b_global_full(dev, orc, sg):
+    r = Run(sg.VLLM7B, dev, mode=1)
+    w = r.w
+    units = [(l, 0, g) for l in range(w.L) for g in range(w.Hkv)]
+    S = orc.run_units(lambda u: orc.scores_unit(r.unit_kv("K", *u), r.unit_q(*u)), units)
+    s32 = orc.global_scores(S)
+    assert rel_err(s32, r.gs, floor=1e-30) < 1e-4
+    swaps = 0
+    for l in range(r.h):
+        for g in range(w.Hkv):
+            s, _ = r.check_unit(orc, l, 0, g, S32=s32)
+            swaps += s
+    _diag(dict(workload=w.name, mode=1, swaps=swaps))
+
+
+# -------------------------------------------------- full sizes, sampled units
+def _sample_units(r):
+    w = r.w
+    bs = sorted({0, w.B - 1, int(np.argmin(r.n)), int(np.argmax(r.n))})
+    ls = sorted({0, r.h // 2, r.h - 1})
+    out = []
+    for i, b in enumerate(bs):
+        for j, l in enumerate(ls):
+            out.append((l, b, (i + j) % w.Hkv))
+    return out
+
+
+@pytest.mark.parametrize("name", ["longvideo", "vllm72b", "batched"])
+def test_full_size_sampled(dev, orc, sg, name):
+    r = Run(sg.WORKLOADS[name], dev)
+    r.check_all_layer_head(orc, _sample_units(r))
+    # properties over every unit: counts, ordering, bit copies of kept keys
+    w = r.w
+    for l in range(r.h):
+        for b in range(w.B):
+            for g in range(w.Hkv):
+                kept, drop, krows, _ = r.gpu_unit(l, b, g)
+                k, ns = r.k[b * w.L + l], r.ns[b * w.L + l]
+                assert len(kept) == k and len(drop) == ns - k
+                assert np.all(np.diff(kept) > 0)
+                if g == 0 and b == 0 and l % 5 == 0:
+                    np.testing.assert_array_equal(krows, r.unit_kv("K", l, b, g)[kept])
+                # the kept set is the exact top-k of the GPU's own scores
+                S = r.gpu_scores(l, b, g)
+                assert check_sets(S, k, ns, kept, drop) == 0
+
+
+@pytest.mark.parametrize("name", ["longvideo", "vllm72b", "batched"])
+def test_full_size_global_properties(dev, orc, sg, name):
+    r = Run(sg.WORKLOADS[name], dev, mode=1)
+    w = r.w
+    ntot = int(r.toff[-1])
+    # shared score = fixed-order sum of the per-unit scores
+    ref = np.zeros(ntot)
+    for l in range(w.L):
+        for b in range(w.B):
+            for g in range(w.Hkv):
+                nb = r.n[b]
+                ref[r.toff[b]:r.toff[b] + nb] += r.gpu_scores(l, b, g)
+    assert rel_err(ref, r.gs, floor=1e-30) < 1e-6
+    # sampled per-unit scores against the oracle
+    for (l, b, g) in _sample_units(r)[:3]:
+        S32 = orc.scores_unit(r.unit_kv("K", l, b, g), r.unit_q(l, b, g))
+        assert rel_err(S32, r.gpu_scores(l, b, g), floor=1e-30) < 1e-4
+    # selection is the exact top-k of the shared score, for every unit
+    for b in range(w.B):
+        gs = r.gs[r.toff[b]:r.toff[b] + r.n[b]]
+        for l in range(r.h):
+            for g in range(w.Hkv):
+                kept, drop, _, _ = r.gpu_unit(l, b, g)
+                assert check_sets(gs, r.k[b * w.L + l], r.ns[b * w.L + l], kept, drop) == 0
+    # fused values of sampled units against the oracle on the GPU's sets
+    for (l, b, g) in _sample_units(r)[:4]:
+        kept, drop, krows, vrows = r.gpu_unit(l, b, g)
+        V = r.unit_kv("V", l, b, g)
+        ref = orc.fuse(V, kept.astype(np.int32), drop.astype(np.int32))
+        assert fused_error(ref, vrows) <= TOL_BF16
+        np.testing.assert_array_equal(krows, r.unit_kv("K", l, b, g)[kept])
