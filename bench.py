@@ -1,0 +1,298 @@
+#!/usr/bin/env python3
+"""PruneKV benchmark on one MI355X.
+
+One step = one viscache_prune call over the whole visual KV cache of the
+7B-shaped workload (28 layers, 28 query / 4 kv heads, head dim 128, 16 frames x
+196 tokens, 64-token window, overall retention 28%): window scores, budgets,
+keep/drop selection, key gather and value fusion.  Inputs are resident in HBM
+before timing starts; L2 and the 256 MB Infinity Cache are flushed before every
+step by writing a 1 GiB buffer (outside the timed region), because the 180 MB
+input would otherwise be served from the Infinity Cache.
+
+Prints one JSON line: compression throughput (GB of input visual K+V per second)
+with the roofline of the dominant kernel, decode-attention latency per step on
+the full, pruned and empty (no visual rows) caches, and the CPU oracle timed
+on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix peak
+STAGES = ["upload", "score_stats", "score_colsum", "score_shared", "select", "gather_fuse"]
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="vllm7b")
+    ap.add_argument("--rank-mode", default="layer_head", choices=["layer_head", "global"])
+    ap.add_argument("--decode-steps", type=int, default=None)
+    ap.add_argument("--no-flush", action="store_true", help="keep caches warm between steps")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--cpu-units", type=int, default=48, help="oracle units in the CPU sample")
+    return ap.parse_args()
+
+
+def algorithmic(w, pc, n_list):
+    """Per-launch algorithmic work of each stage (bytes, MFMA flops, exps)."""
+    L, Hq, Hkv, d, W, G = w.L, w.Hq, w.Hkv, w.d, w.W, w.G
+    R = G * W
+    Ls = pc.h if pc.params.rank_mode == 0 else L
+    out = {}
+    k_bytes = sum(Hkv * n * d * 2 for n in n_list) * Ls
+    q_bytes = w.B * Hq * W * d * 4 * Ls
+    flops = sum(Hkv * 2 * R * n * d for n in n_list) * Ls
+    exps = sum(Hkv * R * n for n in n_list) * Ls
+    out["score_stats"] = dict(bytes=k_bytes + q_bytes, flops=flops, exps=exps)
+    out["score_colsum"] = dict(bytes=k_bytes + q_bytes // 2, flops=flops, exps=exps)
+    fb, ff, fe = 0, 0, 0
+    for b, n in enumerate(n_list):
+        for l in range(pc.h):
+            k, ns = pc.k[b * L + l], pc.n_surv[b * L + l]
+            r = ns - k
+            fb += Hkv * (ns * d * 2 + k * d * 2 + k * (2 * d * 2 + 4))
+            ff += Hkv * 4 * k * r * d
+            fe += Hkv * k * r
+    out["gather_fuse"] = dict(bytes=fb, flops=ff, exps=fe)
+    out["select"] = dict(bytes=sum(Hkv * n * 4 for n in n_list) * pc.h, flops=0, exps=0)
+    # whole-path algorithmic bytes: K of scored layers, Q, V of survivors, outputs
+    out["path_bytes"] = k_bytes + q_bytes + fb
+    return out
+
+
+def time_prune(pc, steps, warmup, flush_buf, torch):
+    for _ in range(warmup):
+        if flush_buf is not None:
+            flush_buf.fill_(1)
+        pc.run()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(steps):
+        if flush_buf is not None:
+            flush_buf.fill_(s & 0x7F)  # evicts L2 and the Infinity Cache; not timed
+        pc.run(events=ev[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    tot = [e[0].elapsed_time(e[6]) for e in ev]
+    stage = [[e[i].elapsed_time(e[i + 1]) for i in range(6)] for e in ev]
+    return tot, stage, wall
+
+
+def decode_latency(w, pc, dev, steps, flush_buf, torch, sg):
+    """Per-step latency of append + attention over all layers, on the full,
+    pruned and empty-visual caches."""
+    from paper_2608_24063_amd.tensors import DecodeCache
+    from synthgen.device import bf16_tensor
+    L, B, Hkv, d = w.L, w.B, w.Hkv, w.d
+    n = [int(x) for x in w.n_vis()]
+    results = {}
+    text_k = bf16_tensor(sg.normal_bf16(w.seed, 901, (L * B * Hkv, w.W, d)), dev)
+    text_v = bf16_tensor(sg.normal_bf16(w.seed, 902, (L * B * Hkv, w.W, d)), dev)
+    kn = bf16_tensor(sg.normal_bf16(w.seed, 903, (steps, L, B, Hkv, d)), dev)
+    vn = bf16_tensor(sg.normal_bf16(w.seed, 904, (steps, L, B, Hkv, d)), dev)
+    q = bf16_tensor(sg.normal_bf16(w.seed, 905, (steps, L, B, w.Hq, d)), dev)
+    out = torch.empty((L, B, w.Hq, d), dtype=torch.float32, device=dev)
+    for variant in ("full", "pruned", "empty"):
+        vis = []
+        for l in range(L):
+            for b in range(B):
+                for g in range(Hkv):
+                    if variant == "full":
+                        vis.append(n[b])
+                    elif variant == "pruned":
+                        vis.append(pc.k[b * L + l])
+                    else:
+                        vis.append(0)
+        caps = [v + w.W + steps for v in vis]
+        c = DecodeCache(L, B, w.Hq, Hkv, d, caps, dev)
+        lens = []
+        toff = [0]
+        for x in n:
+            toff.append(toff[-1] + x)
+        for l in range(L):
+            for b in range(B):
+                for g in range(Hkv):
+                    u = (l * B + b) * Hkv + g
+                    r0, v = c.offs_host[u], vis[u]
+                    if variant == "full" and v:
+                        s0 = toff[b] * Hkv + g * n[b]
+                        c.k_pool[r0:r0 + v] = pc.k_in[l][s0:s0 + v]
+                        c.v_pool[r0:r0 + v] = pc.v_in[l][s0:s0 + v]
+                    elif variant == "pruned" and v:
+                        a0, a1 = pc.unit_rows(l, b, g)
+                        c.k_pool[r0:r0 + v] = pc.k_out[l][a0:a1]
+                        c.v_pool[r0:r0 + v] = pc.v_out[l][a0:a1]
+                    c.k_pool[r0 + v:r0 + v + w.W] = text_k[u]
+                    c.v_pool[r0 + v:r0 + v + w.W] = text_v[u]
+                    lens.append(v + w.W)
+        c.len.copy_(torch.tensor(lens, dtype=torch.int32))
+        rows0 = sum(lens)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(steps)]
+        # one warm-up step on a copy of the lengths, then restore
+        torch.cuda.synchronize()
+        for t in range(steps):
+            if flush_buf is not None:
+                flush_buf.fill_(t & 0x7F)
+            ev[t][0].record()
+            c.append(kn[t], vn[t])
+            c.attend(q[t], out, d ** -0.5)
+            ev[t][1].record()
+        torch.cuda.synchronize()
+        ts = sorted(a.elapsed_time(b) * 1e3 for a, b in ev)
+        bytes_step0 = (rows0 + len(lens)) * d * 2 * 2
+        results[variant] = dict(mean_us=sum(ts) / len(ts), median_us=ts[len(ts) // 2],
+                                rows=rows0, bytes_per_step=bytes_step0)
+        del c
+    full, pr, em = results["full"], results["pruned"], results["empty"]
+    rho = pr["bytes_per_step"] / full["bytes_per_step"]
+    bound = rho * full["median_us"] + em["median_us"]
+    return dict(steps=steps, full_us=full["median_us"], pruned_us=pr["median_us"], empty_us=em["median_us"],
+                full_mean_us=full["mean_us"], pruned_mean_us=pr["mean_us"],
+                speedup=full["median_us"] / pr["median_us"], rho=rho,
+                target_speedup=full["median_us"] / bound, meets_target=pr["median_us"] <= bound,
+                full_hbm_gbs=full["bytes_per_step"] / (full["median_us"] * 1e3),
+                pruned_hbm_gbs=pr["bytes_per_step"] / (pr["median_us"] * 1e3),
+                cold=flush_buf is not None)
+
+
+def cpu_baseline(w, pc, host, units_wanted):
+    """The oracle on a bounded sample of the same workload: whole units
+    (score, select, gather, fuse) of layer/head ranking, one unit per thread."""
+    import oracle as orc
+    threads = min(16, os.cpu_count() or 1)
+    L, Hkv = w.L, w.Hkv
+    n = [int(x) for x in w.n_vis()]
+    toff = [0]
+    for x in n:
+        toff.append(toff[-1] + x)
+    allu = [(l, b, g) for l in range(pc.h) for b in range(w.B) for g in range(Hkv)]
+    step = max(1, len(allu) // units_wanted)
+    units = allu[::step][:units_wanted]
+
+    def one(u):
+        l, b, g = u
+        s0 = toff[b] * Hkv + g * n[b]
+        K = host["K"][l][s0:s0 + n[b]]
+        V = host["V"][l][s0:s0 + n[b]]
+        Q = host["Q"][l][b, g * w.G:(g + 1) * w.G].reshape(-1, w.d)
+        orc.prune_unit(K, V, Q, pc.k[b * L + l], pc.n_surv[b * L + l])
+        return 1
+
+    t0 = time.perf_counter()
+    orc.run_units(one, units, threads=threads)
+    wall = time.perf_counter() - t0
+    # whole-workload time at the same per-unit rate and thread count
+    t_full = wall * len(allu) / len(units)
+    in_bytes = sum(Hkv * x * w.d * 2 * 2 for x in n) * L
+    return dict(value=in_bytes / t_full / 1e9, unit="GB/s", cores=threads, kind="oracle",
+                sample=f"{len(units)} of {len(allu)} (layer, kv head) units, whole path per unit, "
+                       f"{wall:.1f} s wall on {threads} threads; scaled to the full workload",
+                full_workload_s=t_full)
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}, WORLD_SIZE={world}).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2608_24063_amd as vc
+    import synthgen as sg
+    from paper_2608_24063_amd.tensors import PruneCall
+    from synthgen.device import upload_layers
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    vc.lib()
+    w = sg.WORKLOADS[args.workload]
+    mode = vc.VC_RANK_GLOBAL if args.rank_mode == "global" else vc.VC_RANK_LAYER_HEAD
+    n = [int(x) for x in w.n_vis()]
+    print(f"[bench] generating {w.name}: B={w.B} L={w.L} Hq={w.Hq} Hkv={w.Hkv} d={w.d} W={w.W} n={n[:4]}",
+          file=sys.stderr, flush=True)
+    keep_host = not args.no_cpu_baseline
+    dv, host = upload_layers(w, range(w.L), dev, keep_host=keep_host)
+    params = vc.make_params(w.retention, rank_mode=mode)
+    pc = PruneCall(w.B, w.L, w.Hq, w.Hkv, w.d, w.W, n, params, [dv["K"][l] for l in range(w.L)],
+                   [dv["V"][l] for l in range(w.L)], [dv["Q"][l] for l in range(w.L)])
+    flush = None if args.no_flush else torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    print(f"[bench] timing {args.steps} prune steps after {args.warmup} warm-up", file=sys.stderr, flush=True)
+    tot, stage, wall = time_prune(pc, args.steps, args.warmup, flush, torch)
+    ms = sum(tot) / len(tot)
+    in_bytes = sum(w.Hkv * x * w.d * 2 * 2 for x in n) * w.L
+    alg = algorithmic(w, pc, n)
+    stage_us = {STAGES[i]: 1e3 * sum(s[i] for s in stage) / len(stage) for i in range(6)}
+    dom = max(("score_stats", "score_colsum", "select", "gather_fuse"), key=lambda s: stage_us[s])
+    a = alg[dom]
+    t = stage_us[dom] * 1e-6
+    fr_hbm = a["bytes"] / t / 1e9 / HBM_PEAK_GBS
+    fr_mfma = a["flops"] / t / 1e12 / MFMA_BF16_PEAK_TFLOPS
+    if fr_mfma >= fr_hbm:
+        roof = dict(bound="mfma", achieved=a["flops"] / t / 1e12, peak=MFMA_BF16_PEAK_TFLOPS, unit="TFLOP/s")
+    else:
+        roof = dict(bound="hbm", achieved=a["bytes"] / t / 1e9, peak=HBM_PEAK_GBS, unit="GB/s")
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    roof["kernel"] = dom
+    roof["kernel_us"] = stage_us[dom]
+    roof["hbm_frac"] = fr_hbm
+    roof["mfma_frac"] = fr_mfma
+    roof["exp_per_s"] = a["exps"] / t
+
+    dec = None
+    if not args.no_decode:
+        dsteps = args.decode_steps or w.decode_steps
+        print(f"[bench] decode: {dsteps} steps x 3 caches", file=sys.stderr, flush=True)
+        dec = decode_latency(w, pc, dev, dsteps, flush, torch, sg)
+    cpu = None
+    if not args.no_cpu_baseline:
+        print(f"[bench] CPU oracle sample ({args.cpu_units} units)", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, pc, host, args.cpu_units)
+
+    rec = {
+        "metric": "PruneKV compress GB/s (% of HBM peak) + decode-attn speedup vs full KV",
+        "value": in_bytes / (ms * 1e-3) / 1e9,
+        "unit": "GB/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: B={w.B} L={w.L} Hq={w.Hq} Hkv={w.Hkv} d={w.d} "
+                               f"{w.frames}x{w.tokens_per_frame} visual tokens, W={w.W}, RR={w.retention}",
+                   "rank_mode": args.rank_mode, "cold_caches": flush is not None,
+                   "input_visual_kv_bytes": in_bytes},
+        "hbm_frac_path": alg["path_bytes"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "path_alg_bytes": alg["path_bytes"],
+        "stage_us": stage_us,
+        "ms_per_step_median": sorted(tot)[len(tot) // 2],
+        "wall_s_timed_region": wall,
+        "roofline": roof,
+        "decode": dec,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec))
+
+
+if __name__ == "__main__":
+    main()
