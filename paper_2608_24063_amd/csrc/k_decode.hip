@@ -18,6 +18,7 @@ namespace vc {
 namespace {
 
 constexpr float kNegInf = -__builtin_inff();
+constexpr float kFloor = -1e30f;
 constexpr int kRowTile = 32;
 
 __global__ __launch_bounds__(64) void k_append(int32_t units, int32_t d, uint16_t *k_pool,
@@ -26,21 +27,21 @@ __global__ __launch_bounds__(64) void k_append(int32_t units, int32_t d, uint16_
                                                const uint16_t *k_new, const uint16_t *v_new) {
   const int u = blockIdx.x;
   const int t = threadIdx.x;
-  const int L0 = len[u];
-  const bool room = L0 < cap[u];
+  const int L0 = ldg(len + u);
+  const bool room = L0 < ldg(cap + u);
   const int chunks = d / 8;
   if (room) {
-    const int64_t dst = (row_off[u] + L0) * d;
+    const int64_t dst = (ldg(row_off + u) + L0) * d;
     for (int c = t; c < 2 * chunks; c += 64) {
       const bool isv = c >= chunks;
       const int cc = isv ? c - chunks : c;
       const uint16_t *src = (isv ? v_new : k_new) + (int64_t)u * d + cc * 8;
       uint16_t *dp = (isv ? v_pool : k_pool) + dst + cc * 8;
-      *reinterpret_cast<u32x4 *>(dp) = *reinterpret_cast<const u32x4 *>(src);
+      st16(dp, ld16(src));
     }
   }
   __syncthreads();  // every thread has read len before it moves
-  if (t == 0 && room) len[u] = L0 + 1;
+  if (t == 0 && room) stg(len + u, L0 + 1);
 }
 
 __device__ __forceinline__ bf16x8 load_split8(const uint16_t *row, int c) {
@@ -61,7 +62,7 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
   const uint32_t lb = xcd_block(blockIdx.x, gridDim.x);
   const int split = lb % p.nsplit;
   const int u = lb / p.nsplit;
-  const int len = min(p.len[u], p.cap[u]);
+  const int len = min(ldg(p.len + u), ldg(p.cap + u));
   const int r0 = split * p.split_rows;
   if (r0 >= len && split > 0) return;  // uniform: nothing for this split
   const int r1 = min(len, r0 + p.split_rows);
@@ -69,8 +70,9 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
   const int lr = lane & 15, lg = lane >> 4;
   const int g = u % p.Hkv;
   const int lb_ = u / p.Hkv;  // l * B + b
-  const uint16_t *Kp = p.k_pool + p.row_off[u] * D;
-  const uint16_t *Vp = p.v_pool + p.row_off[u] * D;
+  const int64_t roff = ldg(p.row_off + u);
+  const uint16_t *Kp = p.k_pool + roff * D;
+  const uint16_t *Vp = p.v_pool + roff * D;
 
   // Query heads g*G + lr as B operands (natural k order: 8 consecutive d).
   bf16x8 bq[KS];
@@ -78,14 +80,16 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
 #pragma unroll
   for (int s = 0; s < KS; ++s) {
     u32x4 v = {0, 0, 0, 0};
-    if (lr < p.G) v = *reinterpret_cast<const u32x4 *>(q + 32 * s + 8 * lg);
+    if (lr < p.G) v = ld16(q + 32 * s + 8 * lg);
     bq[s] = as_bf16x8(v);
   }
 
   f32x4 O[MB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) O[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float mrow = kNegInf, lsum = 0.f;
+  // Running max per head, pre-multiplied by the exp2 scale; starts at a finite
+  // floor so rescaling never forms (-inf) - (-inf).
+  float mrow = kFloor, lsum = 0.f;
   const float sc = p.sc;
   uint16_t *myvt = vt[w];
 
@@ -101,7 +105,7 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
         u32x4 a = {0, 0, 0, 0};
-        if (row < r1) a = *reinterpret_cast<const u32x4 *>(Kp + (int64_t)row * D + 32 * s + 8 * lg);
+        if (row < r1) a = ld16(Kp + (int64_t)row * D + 32 * s + 8 * lg);
         acc[rb] = mfma_bf16(as_bf16x8(a), bq[s], acc[rb]);
       }
     }
@@ -113,8 +117,8 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
         const int c = (lane >> 4) + 4 * it;  // 16-byte chunk of the row
         const int ra = t0 + 2 * pp, rb2 = ra + 1;
         u32x4 va = {0, 0, 0, 0}, vb = {0, 0, 0, 0};
-        if (ra < r1) va = *reinterpret_cast<const u32x4 *>(Vp + (int64_t)ra * D + c * 8);
-        if (rb2 < r1) vb = *reinterpret_cast<const u32x4 *>(Vp + (int64_t)rb2 * D + c * 8);
+        if (ra < r1) va = ld16(Vp + (int64_t)ra * D + c * 8);
+        if (rb2 < r1) vb = ld16(Vp + (int64_t)rb2 * D + c * 8);
         const uint32_t ea[4] = {va.x, va.y, va.z, va.w}, eb[4] = {vb.x, vb.y, vb.z, vb.w};
 #pragma unroll
         for (int qq = 0; qq < 4; ++qq) {
@@ -136,13 +140,12 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
       }
     tm = fmaxf(tm, shfl_xor(tm, 16));
     tm = fmaxf(tm, shfl_xor(tm, 32));
-    const float mnew = fmaxf(mrow, tm);
-    const float alpha = (mrow == kNegInf) ? 0.f : fast_exp2(mrow * sc - mnew * sc);
-    mrow = mnew;
+    const float mc = fmaxf(mrow, tm * sc);
+    const float alpha = fast_exp2(mrow - mc);
+    mrow = mc;
     lsum *= alpha;
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) O[mb] *= alpha;
-    const float mc = mnew * sc;
     float pr[2][4];
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb)
@@ -172,7 +175,7 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
   // Merge the four waves, then store this split's partial.
   lsum += shfl_xor(lsum, 16);
   lsum += shfl_xor(lsum, 32);
-  if (lg == 0) wml[w][lr] = make_float2(mrow, lsum);
+  if (lg == 0) wml[w][lr] = make_float2(mrow <= kFloor ? kNegInf : mrow, lsum);
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -190,14 +193,14 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
       for (int i = 0; i < 4; ++i) {
         const float2 ml = wml[i][h];
         if (ml.x != kNegInf) {
-          const float f = fast_exp2(ml.x * sc - M * sc);
+          const float f = fast_exp2(ml.x - M);
           o += f * wo[i][h][x];
           s += f * ml.y;
         }
       }
     }
-    p.part_o[(pbase + h) * D + x] = o;
-    if (x == 0) p.part_ml[pbase + h] = make_float2(M, s);
+    stg(p.part_o + (pbase + h) * D + x, o);
+    if (x == 0) stg(p.part_ml + pbase + h, make_float2(M, s));
   }
 }
 
@@ -205,7 +208,7 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
 template <int D>
 __global__ __launch_bounds__(256) void k_decode_combine(DecodePlan p) {
   const int u = blockIdx.x;
-  const int len = min(p.len[u], p.cap[u]);
+  const int len = min(ldg(p.len + u), ldg(p.cap + u));
   const int ns = len > 0 ? min(p.nsplit, (len + p.split_rows - 1) / p.split_rows) : 1;
   const int g = u % p.Hkv;
   const int lb_ = u / p.Hkv;
@@ -213,19 +216,19 @@ __global__ __launch_bounds__(256) void k_decode_combine(DecodePlan p) {
   for (int e = threadIdx.x; e < p.G * D; e += 256) {
     const int h = e / D, x = e % D;
     float M = kNegInf;
-    for (int s = 0; s < ns; ++s) M = fmaxf(M, p.part_ml[((int64_t)u * p.nsplit + s) * 16 + h].x);
+    for (int s = 0; s < ns; ++s) M = fmaxf(M, ldg(p.part_ml + ((int64_t)u * p.nsplit + s) * 16 + h).x);
     float o = 0.f, sum = 0.f;
     if (M != kNegInf) {
       for (int s = 0; s < ns; ++s) {
         const int64_t pb = ((int64_t)u * p.nsplit + s) * 16 + h;
-        const float2 ml = p.part_ml[pb];
+        const float2 ml = ldg(p.part_ml + pb);
         if (ml.x == kNegInf) continue;
-        const float f = fast_exp2(ml.x * sc - M * sc);
-        o += f * p.part_o[pb * D + x];
+        const float f = fast_exp2(ml.x - M);
+        o += f * ldg(p.part_o + pb * D + x);
         sum += f * ml.y;
       }
     }
-    p.out[((int64_t)lb_ * p.Hq + (int64_t)g * p.G + h) * D + x] = sum > 0.f ? o / sum : 0.f;
+    stg(p.out + ((int64_t)lb_ * p.Hq + (int64_t)g * p.G + h) * D + x, sum > 0.f ? o / sum : 0.f);
   }
 }
 

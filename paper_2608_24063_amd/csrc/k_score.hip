@@ -12,9 +12,31 @@ namespace vc {
 namespace {
 
 constexpr float kNegInf = -__builtin_inff();
+// Running maxima are kept already multiplied by the exp2 scale, so every
+// rescale factor is exp2 of a plain difference of two floats (no product that
+// the compiler could contract into an inexact fma).  They start at a finite
+// floor, so rescaling never computes (-inf) - (-inf): exp2(floor - real max)
+// underflows to 0 and exp2(floor - floor) is 1.
+constexpr float kFloor = -1e30f;
 
-// Stage a tile of 64 rows x D bf16 (rows [r0, r0+64) of `src`, rows >= rmax
-// read as zero) into registers; the whole workgroup participates.
+// LDS row pitch of staged K / Q tiles: 32 bytes of padding keeps rows 16-byte
+// aligned and measured free of bank conflicts for the 16-byte operand reads.
+template <int D>
+constexpr int kPitch = D + 16;
+
+// Interleave hints for the scheduler: alternate one matrix instruction with
+// `v` vector instructions, `n` times.
+template <int n, int v>
+__device__ __forceinline__ void interleave_mfma_valu() {
+#pragma unroll
+  for (int i = 0; i < n; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, v, 0);
+  }
+}
+
+// A tile of 64 rows x D bf16 staged through registers into LDS; rows past
+// `rmax` read as zero.  The whole workgroup (256 threads) participates.
 template <int D>
 struct TileRegs {
   static constexpr int kChunks = 64 * D / 8 / 256;  // 16-byte chunks per thread
@@ -22,21 +44,18 @@ struct TileRegs {
   __device__ __forceinline__ void load(const uint16_t *src, int64_t r0, int64_t rmax, int tid) {
 #pragma unroll
     for (int i = 0; i < kChunks; ++i) {
-      int c = tid + i * 256;
-      int row = c / (D / 8), col = c % (D / 8);
-      int64_t gr = r0 + row;
-      if (gr < rmax)
-        v[i] = *reinterpret_cast<const u32x4 *>(src + gr * D + col * 8);
-      else
-        v[i] = u32x4{0, 0, 0, 0};
+      const int c = tid + i * 256;
+      const int row = c / (D / 8), col = c % (D / 8);
+      const int64_t gr = r0 + row;
+      v[i] = gr < rmax ? ld16(src + gr * D + col * 8) : u32x4{0, 0, 0, 0};
     }
   }
   __device__ __forceinline__ void store(uint16_t *lds, int tid) const {
-    constexpr int P = D + 8;
+    constexpr int P = kPitch<D>;
 #pragma unroll
     for (int i = 0; i < kChunks; ++i) {
-      int c = tid + i * 256;
-      int row = c / (D / 8), col = c % (D / 8);
+      const int c = tid + i * 256;
+      const int row = c / (D / 8), col = c % (D / 8);
       *reinterpret_cast<u32x4 *>(lds + row * P + col * 8) = v[i];
     }
   }
@@ -48,28 +67,83 @@ __device__ __forceinline__ void unit_coords(const PrunePlan &p, int u, int &ls, 
   ls = u / (p.Hkv * p.B);
 }
 
-// Merge two (max, sum) pairs whose sums are relative to exp2(max * sc).
-__device__ __forceinline__ void merge_stats(float &m, float &s, float mo, float so, float sc) {
-  float M = fmaxf(m, mo);
-  if (M == kNegInf) return;  // both empty
-  float Mc = M * sc;
-  float a = (m == kNegInf) ? 0.f : s * fast_exp2(m * sc - Mc);
-  float c = (mo == kNegInf) ? 0.f : so * fast_exp2(mo * sc - Mc);
-  m = M;
-  s = a + c;
-}
-
 // ---------------------------------------------------------------------------
 // Pass 1: row statistics.  Workgroup = (unit, 256-row query group, key split).
 // Wave w owns query rows qg*256 + w*64 + [0, 64) as MFMA B operands and all
 // four waves share each 64-key tile of K staged in LDS (A operands), so the
 // product is Z^T (keys x queries): lane l sees query l%16 of each 16-row block
-// and keys 4*(l/16)+i, and keeps running (max, sum) per query in registers.
+// and keys 4*(l/16)+i, and keeps a running (max, sum) per query in registers.
 // ---------------------------------------------------------------------------
+// Softmax statistics of one 16-row query block (lane's row: qb*16 + l%16)
+// over the 64 keys of a tile.
+template <bool MASK>
+__device__ __forceinline__ void stats_rows(f32x4 (&acc)[4], float &m, float &sum, int tb, int k1,
+                                           int lg, float sc) {
+  if (MASK) {
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (tb + kb * 16 + 4 * lg + i >= k1) acc[kb][i] = kNegInf;
+  }
+  float tm = acc[0][0];
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) tm = fmaxf(tm, acc[kb][i]);
+  const float mnew = fmaxf(m, tm * sc);  // scaled running max
+  float part = 0.f;
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) part += fast_exp2(fmaf(acc[kb][i], sc, -mnew));
+  sum = fmaf(sum, fast_exp2(m - mnew), part);
+  m = mnew;
+}
+
+// One 64-key tile against the wave's four 16-row query blocks.  The K tile's
+// operands are read from LDS once; the matrix work of block qb+1 is issued
+// ahead of the softmax work of block qb so the two units overlap.
+template <int D, bool MASK>
+__device__ __forceinline__ void stats_tile(const uint16_t *kl, const bf16x8 (&bq)[4][D / 32],
+                                           float (&m)[4], float (&sum)[4], int tb, int k1, int lr,
+                                           int lg, float sc) {
+  constexpr int KS = D / 32;
+  constexpr int P = kPitch<D>;
+  bf16x8 a[4][KS];
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      a[kb][s] = as_bf16x8(*reinterpret_cast<const u32x4 *>(kl + (kb * 16 + lr) * P + 32 * s + 8 * lg));
+  f32x4 cur[4], nxt[4];
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) {
+    cur[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) cur[kb] = mfma_bf16(a[kb][s], bq[0][s], cur[kb]);
+  }
+#pragma unroll
+  for (int qb = 0; qb < 4; ++qb) {
+    if (qb + 1 < 4) {
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        nxt[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < KS; ++s) nxt[kb] = mfma_bf16(a[kb][s], bq[qb + 1][s], nxt[kb]);
+      }
+    }
+    stats_rows<MASK>(cur, m[qb], sum[qb], tb, k1, lg, sc);
+    if (qb + 1 < 4) interleave_mfma_valu<4 * KS, 4>();
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) cur[kb] = nxt[kb];
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p) {
   constexpr int KS = D / 32;
-  constexpr int P = D + 8;
+  constexpr int P = kPitch<D>;
   __shared__ __attribute__((aligned(16))) uint16_t kt[2][kKeyTile * P];
 
   const uint32_t lb = xcd_block(blockIdx.x, gridDim.x);
@@ -78,7 +152,8 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p) {
   const int u = lb / (p.nqg * p.nks);
   int ls, b, g;
   unit_coords(p, u, ls, b, g);
-  const int n = p.nb[b];
+  const int n = ldg(p.nb + b);
+  const int64_t toff = ldg(p.toff + b);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const float sc = p.sc;
@@ -86,10 +161,10 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p) {
   const int span = ((n + p.nks - 1) / p.nks + 15) & ~15;
   const int k0 = min(n, ks * span), k1 = min(n, k0 + span);
 
-  const uint16_t *K = reinterpret_cast<const uint16_t *>(p.lp[LP_K_IN * p.L + ls]) +
-                      ((int64_t)p.toff[b] * p.Hkv + (int64_t)g * n) * D;
+  const uint16_t *K = reinterpret_cast<const uint16_t *>(ldg(p.lp + LP_K_IN * p.L + ls)) +
+                      (toff * p.Hkv + (int64_t)g * n) * D;
   const int64_t qoff = ((int64_t)b * p.Hq + (int64_t)g * p.G) * p.W * D;
-  const float *Q = reinterpret_cast<const float *>(p.lp[LP_Q * p.L + ls]) + qoff;
+  const float *Q = reinterpret_cast<const float *>(ldg(p.lp + LP_Q * p.L + ls)) + qoff;
   uint16_t *Qb = p.qbf + (int64_t)ls * p.B * p.Hq * p.W * D + qoff;
 
   // Query rows -> bf16 B operands (round to nearest even), zero past R.
@@ -102,11 +177,13 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p) {
     for (int s = 0; s < KS; ++s) {
       u32x4 pk = {0, 0, 0, 0};
       if (row < p.R) {
-        const float4 *src = reinterpret_cast<const float4 *>(Q + (int64_t)row * D + 32 * s + 8 * lg);
-        float4 x0 = src[0], x1 = src[1];
-        pk = u32x4{pack_bf16(x0.x, x0.y), pack_bf16(x0.z, x0.w), pack_bf16(x1.x, x1.y),
-                   pack_bf16(x1.z, x1.w)};
-        if (ks == 0) *reinterpret_cast<u32x4 *>(Qb + (int64_t)row * D + 32 * s + 8 * lg) = pk;
+        const float *src = Q + (int64_t)row * D + 32 * s + 8 * lg;
+        const u32x4 a = ld16(src), c = ld16(src + 4);
+        pk = u32x4{pack_bf16(__uint_as_float(a.x), __uint_as_float(a.y)),
+                   pack_bf16(__uint_as_float(a.z), __uint_as_float(a.w)),
+                   pack_bf16(__uint_as_float(c.x), __uint_as_float(c.y)),
+                   pack_bf16(__uint_as_float(c.z), __uint_as_float(c.w))};
+        if (ks == 0) st16(Qb + (int64_t)row * D + 32 * s + 8 * lg, pk);
       }
       bq[qb][s] = as_bf16x8(pk);
     }
@@ -114,7 +191,7 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p) {
 
   float m[4], sum[4];
 #pragma unroll
-  for (int qb = 0; qb < 4; ++qb) { m[qb] = kNegInf; sum[qb] = 0.f; }
+  for (int qb = 0; qb < 4; ++qb) { m[qb] = kFloor; sum[qb] = 0.f; }
 
   const int ntiles = (k1 - k0 + kKeyTile - 1) / kKeyTile;
   TileRegs<D> tr;
@@ -126,48 +203,10 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p) {
   for (int t = 0; t < ntiles; ++t) {
     const int tb = k0 + t * kKeyTile;
     if (t + 1 < ntiles) tr.load(K, tb + kKeyTile, k1, tid);
-    const uint16_t *kl = kt[t & 1];
-    f32x4 acc[4][4];
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-      for (int qb = 0; qb < 4; ++qb) acc[kb][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        bf16x8 a = as_bf16x8(*reinterpret_cast<const u32x4 *>(kl + (kb * 16 + lr) * P + 32 * s + 8 * lg));
-#pragma unroll
-        for (int qb = 0; qb < 4; ++qb) acc[kb][qb] = mfma_bf16(a, bq[qb][s], acc[kb][qb]);
-      }
-    }
-    const bool full = tb + kKeyTile <= k1;
-#pragma unroll
-    for (int qb = 0; qb < 4; ++qb) {
-      float tm = kNegInf;
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float z = acc[kb][qb][i];
-          if (!full && tb + kb * 16 + 4 * lg + i >= k1) z = kNegInf;
-          acc[kb][qb][i] = z;
-          tm = fmaxf(tm, z);
-        }
-      if (tm > m[qb]) {
-        if (m[qb] != kNegInf) sum[qb] *= fast_exp2(m[qb] * sc - tm * sc);
-        m[qb] = tm;
-      }
-      if (m[qb] != kNegInf) {
-        const float mc = m[qb] * sc;
-        float acc_s = 0.f;
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) acc_s += fast_exp2(fmaf(acc[kb][qb][i], sc, -mc));
-        sum[qb] += acc_s;
-      }
-    }
+    if (tb + kKeyTile <= k1)
+      stats_tile<D, false>(kt[t & 1], bq, m, sum, tb, k1, lr, lg, sc);
+    else
+      stats_tile<D, true>(kt[t & 1], bq, m, sum, tb, k1, lr, lg, sc);
     if (t + 1 < ntiles) tr.store(kt[(t + 1) & 1], tid);
     __syncthreads();
   }
@@ -177,13 +216,15 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p) {
   for (int qb = 0; qb < 4; ++qb) {
 #pragma unroll
     for (int mask = 16; mask <= 32; mask <<= 1) {
-      float mo = shfl_xor(m[qb], mask), so = shfl_xor(sum[qb], mask);
-      merge_stats(m[qb], sum[qb], mo, so, sc);
+      const float mo = shfl_xor(m[qb], mask), so = shfl_xor(sum[qb], mask);
+      const float M = fmaxf(m[qb], mo);
+      sum[qb] = sum[qb] * fast_exp2(m[qb] - M) + so * fast_exp2(mo - M);
+      m[qb] = M;
     }
     const int row = row0 + qb * 16 + lr;
     if (lg == 0 && row < p.R) {
-      float mc = m[qb] == kNegInf ? kNegInf : m[qb] * sc;
-      p.part[((int64_t)u * p.nks + ks) * p.R + row] = make_float2(mc, sum[qb]);
+      const float mc = m[qb] <= kFloor ? kNegInf : m[qb];
+      stg(p.part + ((int64_t)u * p.nks + ks) * p.R + row, make_float2(mc, sum[qb]));
     }
   }
 }
@@ -198,106 +239,116 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p) {
 template <int D>
 __global__ __launch_bounds__(256, 2) void k_score_colsum(PrunePlan p) {
   constexpr int KS = D / 32;
-  constexpr int P = D + 8;
+  constexpr int P = kPitch<D>;
   constexpr int kMaxR = 1024;
   __shared__ __attribute__((aligned(16))) uint16_t qt[2][64 * P];
-  __shared__ __attribute__((aligned(16))) float2 rs[kMaxR + 64];
+  __shared__ __attribute__((aligned(16))) float2 rs[kMaxR];
 
   const uint32_t lb = xcd_block(blockIdx.x, gridDim.x);
   const int c = lb % p.ncol;
   const int u = lb / p.ncol;
   int ls, b, g;
   unit_coords(p, u, ls, b, g);
-  const int n = p.nb[b];
+  const int n = ldg(p.nb + b);
   if (c * kColKeys >= n) return;  // whole workgroup exits together
+  const int64_t toff = ldg(p.toff + b);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const float sc = p.sc;
   const int R = p.R;
-
-  // Row statistics: merge the key splits of pass 1.  Rows past R get a
-  // reference of +inf so they contribute exp2(-inf) = 0.
   const int Rpad = (R + 63) & ~63;
-  for (int r = tid; r < Rpad; r += 256) {
-    float2 st = make_float2(__builtin_inff(), 0.f);
-    if (r < R) {
-      float M = kNegInf;
-      for (int k = 0; k < p.nks; ++k) M = fmaxf(M, p.part[((int64_t)u * p.nks + k) * R + r].x);
-      float s = 0.f;
-      if (M != kNegInf)
-        for (int k = 0; k < p.nks; ++k) {
-          float2 q = p.part[((int64_t)u * p.nks + k) * R + r];
-          if (q.x != kNegInf) s += q.y * fast_exp2(q.x - M);
-        }
-      st = make_float2(M == kNegInf ? __builtin_inff() : M, s > 0.f ? 1.f / s : 0.f);
-    }
-    rs[r] = st;
-  }
 
-  const uint16_t *K = reinterpret_cast<const uint16_t *>(p.lp[LP_K_IN * p.L + ls]) +
-                      ((int64_t)p.toff[b] * p.Hkv + (int64_t)g * n) * D;
+  const uint16_t *K = reinterpret_cast<const uint16_t *>(ldg(p.lp + LP_K_IN * p.L + ls)) +
+                      (toff * p.Hkv + (int64_t)g * n) * D;
   const uint16_t *Qb = p.qbf + (int64_t)ls * p.B * p.Hq * p.W * D +
                        ((int64_t)b * p.Hq + (int64_t)g * p.G) * p.W * D;
 
+  // Keys of this wave as B operands.
   const int key0 = c * kColKeys + w * 64;
   bf16x8 bk[4][KS];
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) {
     const int key = key0 + kb * 16 + lr;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      u32x4 v = {0, 0, 0, 0};
-      if (key < n) v = *reinterpret_cast<const u32x4 *>(K + (int64_t)key * D + 32 * s + 8 * lg);
-      bk[kb][s] = as_bf16x8(v);
-    }
+    for (int s = 0; s < KS; ++s)
+      bk[kb][s] = as_bf16x8(key < n ? ld16(K + (int64_t)key * D + 32 * s + 8 * lg) : u32x4{0, 0, 0, 0});
   }
-  float col[4] = {0.f, 0.f, 0.f, 0.f};
-
-  const int ntiles = Rpad / 64;
   TileRegs<D> tr;
   tr.load(Qb, 0, R, tid);
+
+  // Row statistics: merge the key splits of pass 1.  Rows past R get a
+  // reference of +inf so they contribute exp2(-inf) = 0.
+  for (int r = tid; r < Rpad; r += 256) {
+    float2 st = make_float2(__builtin_inff(), 0.f);
+    if (r < R) {
+      const float2 *pr = p.part + (int64_t)u * p.nks * R + r;
+      float M = kNegInf;
+      for (int k = 0; k < p.nks; ++k) M = fmaxf(M, ldg(pr + (int64_t)k * R).x);
+      float s = 0.f;
+      if (M != kNegInf)
+        for (int k = 0; k < p.nks; ++k) {
+          const float2 q = ldg(pr + (int64_t)k * R);
+          if (q.x != kNegInf) s += q.y * fast_exp2(q.x - M);
+        }
+      st = make_float2(M == kNegInf ? __builtin_inff() : M, s > 0.f ? 1.f / s : 0.f);
+    }
+    rs[r] = st;
+  }
   tr.store(qt[0], tid);
   __syncthreads();
+
+  float col[4] = {0.f, 0.f, 0.f, 0.f};
+  const int ntiles = Rpad / 64;
   for (int t = 0; t < ntiles; ++t) {
     if (t + 1 < ntiles) tr.load(Qb, (t + 1) * 64, R, tid);
     const uint16_t *ql = qt[t & 1];
+    // Matrix work of query block qb+1 is issued ahead of the exp work of qb.
+    f32x4 cur[4], nxt[4];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) cur[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const bf16x8 a = as_bf16x8(*reinterpret_cast<const u32x4 *>(ql + lr * P + 32 * s + 8 * lg));
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) cur[kb] = mfma_bf16(a, bk[kb][s], cur[kb]);
+    }
 #pragma unroll
     for (int qb = 0; qb < 4; ++qb) {
-      f32x4 acc[4];
+      if (qb + 1 < 4) {
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) acc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int kb = 0; kb < 4; ++kb) nxt[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        bf16x8 a = as_bf16x8(*reinterpret_cast<const u32x4 *>(ql + (qb * 16 + lr) * P + 32 * s + 8 * lg));
+        for (int s = 0; s < KS; ++s) {
+          const bf16x8 a = as_bf16x8(*reinterpret_cast<const u32x4 *>(ql + ((qb + 1) * 16 + lr) * P + 32 * s + 8 * lg));
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) acc[kb] = mfma_bf16(a, bk[kb][s], acc[kb]);
+          for (int kb = 0; kb < 4; ++kb) nxt[kb] = mfma_bf16(a, bk[kb][s], nxt[kb]);
+        }
       }
       const int rbase = t * 64 + qb * 16 + 4 * lg;
-      float mr[4], ir[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float2 st = rs[rbase + i];
-        mr[i] = st.x;
-        ir[i] = st.y;
-      }
+      const f32x4 s01 = *reinterpret_cast<const f32x4 *>(&rs[rbase]);
+      const f32x4 s23 = *reinterpret_cast<const f32x4 *>(&rs[rbase + 2]);
+      const float mr[4] = {s01.x, s01.z, s23.x, s23.z}, ir[4] = {s01.y, s01.w, s23.y, s23.w};
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          col[kb] = fmaf(fast_exp2(fmaf(acc[kb][i], sc, -mr[i])), ir[i], col[kb]);
+          col[kb] = fmaf(fast_exp2(fmaf(cur[kb][i], sc, -mr[i])), ir[i], col[kb]);
+      if (qb + 1 < 4) interleave_mfma_valu<4 * KS, 3>();
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) cur[kb] = nxt[kb];
     }
     if (t + 1 < ntiles) tr.store(qt[(t + 1) & 1], tid);
     __syncthreads();
   }
 
-  float *S = p.S + (int64_t)ls * p.Ntot * p.Hkv + (int64_t)p.toff[b] * p.Hkv + (int64_t)g * n;
+  float *S = p.S + (int64_t)ls * p.Ntot * p.Hkv + toff * p.Hkv + (int64_t)g * n;
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) {
     float v = col[kb];
     v += shfl_xor(v, 16);
     v += shfl_xor(v, 32);
     const int key = key0 + kb * 16 + lr;
-    if (lg == 0 && key < n) S[key] = v;
+    if (lg == 0 && key < n) stg(S + key, v);
   }
 }
 
@@ -307,15 +358,16 @@ __global__ __launch_bounds__(256) void k_score_global(PrunePlan p) {
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (t >= p.Ntot) return;
   int b = 0;
-  while (b + 1 < p.B && p.toff[b + 1] <= t) ++b;
-  const int64_t v = t - p.toff[b];
-  const int n = p.nb[b];
+  while (b + 1 < p.B && ldg(p.toff + b + 1) <= t) ++b;
+  const int64_t toff = ldg(p.toff + b);
+  const int64_t v = t - toff;
+  const int n = ldg(p.nb + b);
   double acc = 0.0;
   for (int l = 0; l < p.Ls; ++l) {
-    const float *S = p.S + (int64_t)l * p.Ntot * p.Hkv + (int64_t)p.toff[b] * p.Hkv;
-    for (int g = 0; g < p.Hkv; ++g) acc += (double)S[(int64_t)g * n + v];
+    const float *S = p.S + (int64_t)l * p.Ntot * p.Hkv + toff * p.Hkv;
+    for (int g = 0; g < p.Hkv; ++g) acc += (double)ldg(S + (int64_t)g * n + v);
   }
-  p.gs[t] = (float)acc;
+  stg(p.gs + t, (float)acc);
 }
 
 }  // namespace

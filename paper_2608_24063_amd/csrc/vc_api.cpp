@@ -95,7 +95,10 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   const int64_t units = (int64_t)y.Ls * y.B * y.Hkv;
   y.nqg = (y.R + kStatsRows - 1) / kStatsRows;
   const int64_t base = std::max<int64_t>(1, units * y.nqg);
-  int64_t nks = (1024 + base - 1) / base;
+  // Key splits so that the statistics pass runs in one round of resident
+  // workgroups (256 CUs x 2): a second, partial round costs a full workgroup
+  // time for a fraction of the work.
+  int64_t nks = std::max<int64_t>(1, 512 / base);
   nks = std::min<int64_t>(nks, 8);
   nks = std::min<int64_t>(nks, std::max(1, (y.nmax + kKeyTile - 1) / kKeyTile));
   y.nks = (int32_t)std::max<int64_t>(1, nks);

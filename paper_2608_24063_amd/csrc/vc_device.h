@@ -14,6 +14,55 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kLog2e = 1.4426950408889634f;
+
+// Pointers the kernels read from the plan are generic; accesses through them
+// compile to flat instructions, which on gfx9 also count against the LDS wait
+// counter and so stall every LDS read behind in-flight global loads.  All
+// global memory traffic goes through these global-address-space views.
+#define VC_GLOBAL __attribute__((address_space(1)))
+
+template <typename T>
+__device__ __forceinline__ const VC_GLOBAL T *gp(const T *p) {
+  return (const VC_GLOBAL T *)p;
+}
+template <typename T>
+__device__ __forceinline__ VC_GLOBAL T *gp(T *p) {
+  return (VC_GLOBAL T *)p;
+}
+// 16- and 8-byte global loads / stores at element pointer p.
+template <typename T>
+__device__ __forceinline__ u32x4 ld16(const T *p) {
+  return *reinterpret_cast<const VC_GLOBAL u32x4 *>(gp(p));
+}
+template <typename T>
+__device__ __forceinline__ u32x2 ld8(const T *p) {
+  return *reinterpret_cast<const VC_GLOBAL u32x2 *>(gp(p));
+}
+template <typename T>
+__device__ __forceinline__ void st16(T *p, u32x4 v) {
+  *reinterpret_cast<VC_GLOBAL u32x4 *>(gp(p)) = v;
+}
+template <typename T>
+__device__ __forceinline__ void st8(T *p, u32x2 v) {
+  *reinterpret_cast<VC_GLOBAL u32x2 *>(gp(p)) = v;
+}
+template <typename T>
+__device__ __forceinline__ T ldg(const T *p) {
+  return *gp(p);
+}
+template <typename T>
+__device__ __forceinline__ void stg(T *p, T v) {
+  *gp(p) = v;
+}
+// float2 is a class type that cannot be accessed through an address-space
+// qualified reference; move it as two 32-bit words.
+__device__ __forceinline__ float2 ldg(const float2 *p) {
+  const u32x2 v = ld8(p);
+  return make_float2(__uint_as_float(v.x), __uint_as_float(v.y));
+}
+__device__ __forceinline__ void stg(float2 *p, float2 v) {
+  st8(p, u32x2{__float_as_uint(v.x), __float_as_uint(v.y)});
+}
 constexpr int kXcds = 8;  // MI355X: 8 accelerator complex dies, 32 CUs each
 
 // D = A(16x32) * B(32x16) + C on the matrix cores.  Lane l holds row l%16 of A

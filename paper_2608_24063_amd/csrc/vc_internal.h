@@ -14,10 +14,10 @@ enum { LP_K_IN = 0, LP_V_IN, LP_Q, LP_K_OUT, LP_V_OUT, LP_IDX, LP_DROP, LP_COUNT
 constexpr int kStatsRows = 256;   // query rows per stats workgroup (4 waves x 64)
 constexpr int kKeyTile = 64;      // keys staged per LDS tile
 constexpr int kColKeys = 256;     // keys per column-sum workgroup (4 waves x 64)
-constexpr int kFuseRows = 64;     // kept rows per fusion workgroup (4 waves x 16)
+constexpr int kFuseRows = 128;    // kept rows per fusion workgroup (4 waves x 32)
 constexpr int kDropTile = 64;     // dropped rows staged per LDS tile
-constexpr int kSelectThreads = 1024;
-constexpr int kSelectPerThread = 32;  // => n <= 32768 tokens per sequence
+constexpr int kSelectThreads = 512;
+constexpr int kSelectPerThread = 64;  // => n <= 32768 tokens per sequence
 constexpr int kMaxTokens = kSelectThreads * kSelectPerThread;
 
 // Everything the prune kernels need, by value (a few hundred bytes).  Array
