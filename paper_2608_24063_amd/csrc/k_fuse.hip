@@ -14,6 +14,15 @@
 // ends holding kept row l%16, columns 16*mb + 4*(l/16) + i -- the same columns
 // it loaded of V_k, which the mu-blend reuses.  With fp32 output the
 // probabilities enter the second product as a bf16 hi + lo pair.
+//
+// Pipeline per workgroup: dropped-row indices are fetched four tiles ahead,
+// the rows themselves three tiles ahead into two register sets, and staged
+// into one of two LDS buffers one tile ahead; LDS operands of the matrix
+// products are read one k-step ahead.  The running row maximum is only
+// raised when a tile's logits exceed it by more than 2^kSlack, so most tiles
+// skip the cross-lane reduction and the rescale of the accumulators.
+#include <type_traits>
+
 #include "vc_device.h"
 #include "vc_internal.h"
 
@@ -22,6 +31,9 @@ namespace vc {
 namespace {
 
 constexpr float kNegInf = -__builtin_inff();
+// Probabilities are allowed to reach 2^kSlack before the running maximum is
+// raised (and the accumulators rescaled); fp32 has ample range for that.
+constexpr float kSlack = 8.f;
 
 // Row pitch of the staged dropped tile: 32 bytes of padding.  Measured on
 // gfx950, this keeps the transposing reads conflict-free and costs the direct
@@ -47,7 +59,7 @@ __device__ __forceinline__ u32x2 lds_read_tr16(const uint16_t *p) {
 
 // Rows of one 64-row dropped tile between their global load and their LDS
 // store: thread t owns rows 2*(t%32) and 2*(t%32)+1 and the 16-byte chunks
-// (t/32) + 8*it of both.
+// (t/32) + 8*it of both.  Row indices are valid (clamped) token indices.
 template <int D>
 struct DropRegs {
   static constexpr int kIt = D / 64;
@@ -56,8 +68,8 @@ struct DropRegs {
 #pragma unroll
     for (int it = 0; it < kIt; ++it) {
       const int c = c0 + 8 * it;
-      a[it] = ia >= 0 ? ld16(V + (int64_t)ia * D + c * 8) : u32x4{0, 0, 0, 0};
-      b[it] = ib >= 0 ? ld16(V + (int64_t)ib * D + c * 8) : u32x4{0, 0, 0, 0};
+      a[it] = ld16(V + (int64_t)ia * D + c * 8);
+      b[it] = ld16(V + (int64_t)ib * D + c * 8);
     }
   }
   __device__ __forceinline__ void store(uint16_t *vr, int pp, int c0) const {
@@ -72,21 +84,156 @@ struct DropRegs {
   }
 };
 
-// Workgroup = (layer, sequence, kv head, 128 kept rows); wave w owns kept rows
-// w*32 + nb*16 + [0, 16) for nb = 0, 1, so every operand read from LDS feeds
-// two matrix instructions.  Dropped tiles are double-buffered in LDS.
 template <int D>
+struct FuseState {
+  static constexpr int KS = D / 32, MB = D / 16, NB = 2;
+  bf16x8 bvk[NB][KS];  // kept values, B operand of S^T
+  f32x4 O[NB][MB];     // O^T accumulators
+  float mrow[NB];      // running max of the scaled logits (x log2(e)/tau)
+  float lsum[NB];      // this lane's share of the running denominator
+};
+
+// One 64-row dropped tile: S^T, online softmax, O^T.  MASK: the tile has
+// fewer than 64 valid rows (nd).
+template <int D, bool VFP32, bool MASK>
+__device__ __forceinline__ void fuse_tile(FuseState<D> &st, const uint16_t *vt, int nd, float tc, int lr,
+                                          int lg) {
+  constexpr int KS = D / 32, MB = D / 16, NB = 2, PR = kPitchRow<D>;
+
+  // S^T = V_d V_k^T for 64 dropped x 32 kept rows; A operands one k-step ahead.
+  f32x4 acc[NB][4];
+  bf16x8 a[2][4];
+#pragma unroll
+  for (int db = 0; db < 4; ++db) a[0][db] = load_split8_lds(vt + (db * 16 + lr) * PR, 4 * lg);
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    if (s + 1 < KS) {
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+        a[(s + 1) & 1][db] = load_split8_lds(vt + (db * 16 + lr) * PR, 32 * (s + 1) + 4 * lg);
+    }
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        acc[nb][db] = mfma_bf16(a[s & 1][db], st.bvk[nb][s], s == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : acc[nb][db]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  // Transposed V_d operands of the first half of O^T, read while the
+  // softmax runs on the vector unit.
+  const int tr_row = 4 * lg + (lr >> 2), tr_col = 4 * (lr & 3);
+  const uint16_t *tbase = vt + tr_row * PR + tr_col;
+  constexpr int kPre = 4;
+  bf16x8 at[2 * MB];
+#pragma unroll
+  for (int q = 0; q < kPre; ++q) {
+    const uint16_t *b0 = tbase + (32 * (q / MB)) * PR + 16 * (q % MB);
+    const u32x2 lo4 = lds_read_tr16(b0), hi4 = lds_read_tr16(b0 + 16 * PR);
+    at[q] = as_bf16x8(u32x4{lo4.x, lo4.y, hi4.x, hi4.y});
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // Online softmax over dropped rows.  The four lane groups of a kept row
+  // share one running max, raised (wave-uniformly) only when some logit
+  // exceeds it by more than 2^kSlack.
+  float tm[NB];
+  bool grow = false;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    if (MASK) {
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (db * 16 + 4 * lg + i >= nd) acc[nb][db][i] = kNegInf;
+    }
+    float m = acc[nb][0][0];
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) m = fmaxf(m, acc[nb][db][i]);
+    tm[nb] = m * tc;
+    grow |= tm[nb] > st.mrow[nb] + kSlack;
+  }
+  if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      float m = tm[nb];
+      m = fmaxf(m, shfl_xor(m, 16));
+      m = fmaxf(m, shfl_xor(m, 32));
+      const float mc = fmaxf(st.mrow[nb], m);
+      const float alpha = fast_exp2(st.mrow[nb] - mc);
+      st.mrow[nb] = mc;
+      st.lsum[nb] *= alpha;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) st.O[nb][mb] *= alpha;
+    }
+  }
+  bf16x8 bph[NB][2], bpl[NB][2];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    float pr[4][4];
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        pr[db][i] = fast_exp2(fmaf(acc[nb][db][i], tc, -st.mrow[nb]));
+        st.lsum[nb] += pr[db][i];
+      }
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2) {
+      const float *p0 = pr[2 * t2], *p1 = pr[2 * t2 + 1];
+      const u32x4 hi = {pack_bf16(p0[0], p0[1]), pack_bf16(p0[2], p0[3]), pack_bf16(p1[0], p1[1]),
+                        pack_bf16(p1[2], p1[3])};
+      bph[nb][t2] = as_bf16x8(hi);
+      if (VFP32) {
+        const u32x4 lo = {pack_bf16(p0[0] - bf16_lo(hi.x), p0[1] - bf16_hi(hi.x)),
+                          pack_bf16(p0[2] - bf16_lo(hi.y), p0[3] - bf16_hi(hi.y)),
+                          pack_bf16(p1[0] - bf16_lo(hi.z), p1[1] - bf16_hi(hi.z)),
+                          pack_bf16(p1[2] - bf16_lo(hi.w), p1[3] - bf16_hi(hi.w))};
+        bpl[nb][t2] = as_bf16x8(lo);
+      }
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // O^T += V_d^T P^T over two 32-row k-steps, operands kPre reads ahead.
+#pragma unroll
+  for (int q = 0; q < 2 * MB; ++q) {
+    if (q + kPre < 2 * MB) {
+      const int qn = q + kPre;
+      const uint16_t *b0 = tbase + (32 * (qn / MB)) * PR + 16 * (qn % MB);
+      const u32x2 lo4 = lds_read_tr16(b0), hi4 = lds_read_tr16(b0 + 16 * PR);
+      at[qn] = as_bf16x8(u32x4{lo4.x, lo4.y, hi4.x, hi4.y});
+    }
+    const int t2 = q / MB, mb = q % MB;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      st.O[nb][mb] = mfma_bf16(at[q], bph[nb][t2], st.O[nb][mb]);
+      if (VFP32) st.O[nb][mb] = mfma_bf16(at[q], bpl[nb][t2], st.O[nb][mb]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// Workgroup = (fusion unit, 128 kept rows); wave w owns kept rows
+// w*32 + nb*16 + [0, 16) for nb = 0, 1, so every operand read from LDS feeds
+// two matrix instructions.
+template <int D, bool VFP32>
 __global__ __launch_bounds__(256, 2) void k_fuse(PrunePlan p) {
-  constexpr int KS = D / 32;
-  constexpr int MB = D / 16;
-  constexpr int PR = kPitchRow<D>;
-  constexpr int NB = 2;
+  constexpr int KS = D / 32, MB = D / 16, NB = 2, PR = kPitchRow<D>;
   __shared__ __attribute__((aligned(16))) uint16_t vr[2][kDropTile * PR];
   __shared__ int32_t kidx[kFuseRows];
 
-  const uint32_t lb = xcd_block(blockIdx.x, gridDim.x);
-  const int tile = lb % p.nfuse;
-  const int u = lb / p.nfuse;
+  // Block -> (unit, tile): block x*... runs on XCD blockIdx % 8; each XCD
+  // takes every 8th unit of the longest-first list, all tiles of a unit on
+  // the same XCD (they share the unit's dropped rows in L2).
+  const uint32_t x = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
+  const int rank = (int)(x + kXcds * (slot / p.nfuse));
+  const int tile = (int)(slot % p.nfuse);
+  if (rank >= p.nfunits) return;
+  const int u = ldg(p.funit + rank);
   const int g = u % p.Hkv;
   const int b = (u / p.Hkv) % p.B;
   const int l = u / (p.Hkv * p.B);
@@ -110,35 +257,50 @@ __global__ __launch_bounds__(256, 2) void k_fuse(PrunePlan p) {
 
   // Token indices come from the selection kernel; clamping keeps every
   // gathered row inside the unit even if they were corrupted.
-  if (tid < nrows) kidx[tid] = min(max(ldg(idx + j0 + tid), 0), n - 1);
+  auto clampi = [&](int v) { return min(max(v, 0), n - 1); };
+  if (tid < nrows) kidx[tid] = clampi(ldg(idx + j0 + tid));
 
-  // Dropped-tile pipeline: indices one tile ahead of the rows, rows one tile
-  // ahead of the matrix work.
+  // Dropped-tile pipeline.  Indices are read raw and clamped one tile later,
+  // so no wait on them lands right behind the row loads.  Tiles past the end
+  // re-read the last tile (harmless, never consumed).
   const int ntiles = (r + kDropTile - 1) / kDropTile;
   const int pp = tid & 31, c0 = tid >> 5;
-  auto drop_idx = [&](int dt, int row) -> int {
-    const int j = dt * kDropTile + row;
-    return j < r ? min(max(ldg(drop + j), 0), n - 1) : -1;
+  auto raw_idx = [&](int dt, int row) -> int {
+    const int j = min(min(dt, ntiles - 1) * kDropTile + row, r - 1);
+    return ldg(drop + j);
   };
-  DropRegs<D> dr;
-  int ia = -1, ib = -1;
+  DropRegs<D> set0, set1;
+  int pa = 0, pb = 0;  // raw indices of the next tile to load
   if (ntiles > 0) {
-    dr.load(Vin, drop_idx(0, 2 * pp), drop_idx(0, 2 * pp + 1), c0);
-    if (ntiles > 1) { ia = drop_idx(1, 2 * pp); ib = drop_idx(1, 2 * pp + 1); }
-    dr.store(vr[0], pp, c0);
-    if (ntiles > 1) dr.load(Vin, ia, ib, c0);
-    if (ntiles > 2) { ia = drop_idx(2, 2 * pp); ib = drop_idx(2, 2 * pp + 1); }
+    const int a0 = raw_idx(0, 2 * pp), b0 = raw_idx(0, 2 * pp + 1);
+    const int a1 = raw_idx(1, 2 * pp), b1 = raw_idx(1, 2 * pp + 1);
+    const int a2 = raw_idx(2, 2 * pp), b2 = raw_idx(2, 2 * pp + 1);
+    pa = raw_idx(3, 2 * pp);
+    pb = raw_idx(3, 2 * pp + 1);
+    set0.load(Vin, clampi(a0), clampi(b0), c0);
+    set1.load(Vin, clampi(a1), clampi(b1), c0);
+    set0.store(vr[0], pp, c0);
+    set0.load(Vin, clampi(a2), clampi(b2), c0);
   }
   __syncthreads();
 
-  // Key pruning: bit copies of the kept rows.
-  for (int c = tid; c < nrows * (D / 8); c += 256) {
-    const int row = c / (D / 8), col = c % (D / 8);
-    st16(Kout + (int64_t)(j0 + row) * D + col * 8, ld16(Kin + (int64_t)kidx[row] * D + col * 8));
+  // Key pruning: bit copies of the kept rows (loads first, then stores).
+  {
+    constexpr int kChunks = kFuseRows * (D / 8) / 256;
+    u32x4 kc[kChunks];
+#pragma unroll
+    for (int i = 0; i < kChunks; ++i) {
+      const int c = tid + 256 * i, row = c / (D / 8), col = c % (D / 8);
+      kc[i] = ld16(Kin + (int64_t)kidx[row < nrows ? row : 0] * D + col * 8);
+    }
+#pragma unroll
+    for (int i = 0; i < kChunks; ++i) {
+      const int c = tid + 256 * i, row = c / (D / 8), col = c % (D / 8);
+      if (row < nrows) st16(Kout + (int64_t)(j0 + row) * D + col * 8, kc[i]);
+    }
   }
 
-  // Kept values of this lane's rows, in the split k-element order.
-  bf16x8 bvk[NB][KS];
+  FuseState<D> st;
   bool kvalid[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
@@ -147,120 +309,56 @@ __global__ __launch_bounds__(256, 2) void k_fuse(PrunePlan p) {
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       const uint16_t *row = Vin + (int64_t)kidx[kvalid[nb] ? krow : 0] * D + 32 * s + 4 * lg;
-      const u32x2 x = ld8(row), y = ld8(row + 16);
-      bvk[nb][s] = kvalid[nb] ? as_bf16x8(u32x4{x.x, x.y, y.x, y.y}) : as_bf16x8(u32x4{0, 0, 0, 0});
+      const u32x2 x0 = ld8(row), y0 = ld8(row + 16);
+      st.bvk[nb][s] = kvalid[nb] ? as_bf16x8(u32x4{x0.x, x0.y, y0.x, y0.y}) : as_bf16x8(u32x4{0, 0, 0, 0});
     }
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) st.O[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // Running maxima are pre-multiplied by log2(e)/tau; the finite floor makes
+    // the first tile's rescale factor exp2(floor - max) = 0.
+    st.mrow[nb] = -1e30f;
+    st.lsum[nb] = 0.f;
   }
-
-  f32x4 O[NB][MB];
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) O[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // Running maxima kept pre-multiplied by log2(e)/tau: every rescale factor is
-  // exp2 of a plain difference (exp2(floor - max) = 0 on the first tile).
-  float mrow[NB] = {-1e30f, -1e30f}, lsum[NB] = {0.f, 0.f};
   const float tc = p.tc;
-  // Transposing-read address of this lane inside a staged tile: group lane j
-  // points at row j/4 (plus the k-step base) and column 4*(j%4) (plus 16*mb).
-  const int tr_row = 4 * lg + (lr >> 2), tr_col = 4 * (lr & 3);
 
-  for (int dt = 0; dt < ntiles; ++dt) {
-    const uint16_t *vt = vr[dt & 1];
-    const int nd = min(kDropTile, r - dt * kDropTile);
-
-    // S^T = V_d V_k^T for 64 dropped x 32 kept rows.
-    f32x4 acc[NB][4];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-      for (int db = 0; db < 4; ++db) acc[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < KS; ++s)
-#pragma unroll
-      for (int db = 0; db < 4; ++db) {
-        const bf16x8 a = load_split8_lds(vt + (db * 16 + lr) * PR, 32 * s + 4 * lg);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) acc[nb][db] = mfma_bf16(a, bvk[nb][s], acc[nb][db]);
-      }
-
-    // Online softmax over dropped rows; the four lane groups of a kept row
-    // share one running max.
-    float pr[NB][4][4];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      if (nd < kDropTile) {
-#pragma unroll
-        for (int db = 0; db < 4; ++db)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (db * 16 + 4 * lg + i >= nd) acc[nb][db][i] = kNegInf;
-      }
-      float tm = acc[nb][0][0];
-#pragma unroll
-      for (int db = 0; db < 4; ++db)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) tm = fmaxf(tm, acc[nb][db][i]);
-      tm = fmaxf(tm, shfl_xor(tm, 16));
-      tm = fmaxf(tm, shfl_xor(tm, 32));
-      const float mc = fmaxf(mrow[nb], tm * tc);
-      const float alpha = fast_exp2(mrow[nb] - mc);
-      mrow[nb] = mc;
-      lsum[nb] *= alpha;
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) O[nb][mb] *= alpha;
-#pragma unroll
-      for (int db = 0; db < 4; ++db)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          pr[nb][db][i] = fast_exp2(fmaf(acc[nb][db][i], tc, -mc));
-          lsum[nb] += pr[nb][db][i];
-        }
-    }
-
-    // O^T += V_d^T P^T, two 32-row k-steps; V_d^T comes from transposing reads.
-#pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2) {
-      bf16x8 bph[NB], bpl[NB];
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const float *p0 = pr[nb][2 * t2], *p1 = pr[nb][2 * t2 + 1];
-        const u32x4 hi = {pack_bf16(p0[0], p0[1]), pack_bf16(p0[2], p0[3]), pack_bf16(p1[0], p1[1]),
-                          pack_bf16(p1[2], p1[3])};
-        bph[nb] = as_bf16x8(hi);
-        if (p.v_fp32) {
-          const u32x4 lo = {pack_bf16(p0[0] - bf16_lo(hi.x), p0[1] - bf16_hi(hi.x)),
-                            pack_bf16(p0[2] - bf16_lo(hi.y), p0[3] - bf16_hi(hi.y)),
-                            pack_bf16(p1[0] - bf16_lo(hi.z), p1[1] - bf16_hi(hi.z)),
-                            pack_bf16(p1[2] - bf16_lo(hi.w), p1[3] - bf16_hi(hi.w))};
-          bpl[nb] = as_bf16x8(lo);
-        }
-      }
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        const uint16_t *base = vt + (32 * t2 + tr_row) * PR + 16 * mb + tr_col;
-        const u32x2 lo4 = lds_read_tr16(base), hi4 = lds_read_tr16(base + 16 * PR);
-        const bf16x8 a = as_bf16x8(u32x4{lo4.x, lo4.y, hi4.x, hi4.y});
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          O[nb][mb] = mfma_bf16(a, bph[nb], O[nb][mb]);
-          if (p.v_fp32) O[nb][mb] = mfma_bf16(a, bpl[nb], O[nb][mb]);
-        }
-      }
-    }
-
-    // Stage tile dt+1 into the other buffer, then fetch tile dt+2.
-    if (dt + 1 < ntiles) dr.store(vr[(dt + 1) & 1], pp, c0);
-    if (dt + 2 < ntiles) dr.load(Vin, ia, ib, c0);
-    if (dt + 3 < ntiles) { ia = drop_idx(dt + 3, 2 * pp); ib = drop_idx(dt + 3, 2 * pp + 1); }
+  // End of tile t (parity PAR): stage tile t+1 from its register set into
+  // the other LDS buffer, refill that set with tile t+3, fetch indices of
+  // tile t+4, and synchronise.
+  auto advance = [&](auto par, int t) {
+    constexpr int PAR = decltype(par)::value;
+    DropRegs<D> &nx = PAR ? set0 : set1;
+    nx.store(vr[PAR ^ 1], pp, c0);
+    const int na = raw_idx(t + 4, 2 * pp), nb2 = raw_idx(t + 4, 2 * pp + 1);
+    nx.load(Vin, clampi(pa), clampi(pb), c0);
+    pa = na;
+    pb = nb2;
     __syncthreads();
+  };
+  using P0 = std::integral_constant<int, 0>;
+  using P1 = std::integral_constant<int, 1>;
+  const int nfull = r / kDropTile;
+  int t = 0;
+  for (; t + 1 < nfull; t += 2) {
+    fuse_tile<D, VFP32, false>(st, vr[0], kDropTile, tc, lr, lg);
+    advance(P0{}, t);
+    fuse_tile<D, VFP32, false>(st, vr[1], kDropTile, tc, lr, lg);
+    advance(P1{}, t + 1);
+  }
+  if (t < nfull) {
+    fuse_tile<D, VFP32, false>(st, vr[0], kDropTile, tc, lr, lg);
+    advance(P0{}, t);
+    ++t;
+  }
+  if (t < ntiles) {  // partial last tile
+    const int nd = r - t * kDropTile;
+    fuse_tile<D, VFP32, true>(st, vr[t & 1], nd, tc, lr, lg);
   }
 
   const float mu = p.mu, omu = 1.f - p.mu;
   void *vout = reinterpret_cast<void *>(ldg(p.lp + LP_V_OUT * p.L + l));
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    float ls = lsum[nb];
+    float ls = st.lsum[nb];
     ls += shfl_xor(ls, 16);
     ls += shfl_xor(ls, 32);
     if (!kvalid[nb]) continue;
@@ -268,14 +366,14 @@ __global__ __launch_bounds__(256, 2) void k_fuse(PrunePlan p) {
     const int64_t orow_j = orow + j0 + w * 32 + nb * 16 + lr;
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
-      const u32x4 kv = as_u32x4(bvk[nb][mb / 2]);
+      const u32x4 kv = as_u32x4(st.bvk[nb][mb / 2]);
       const uint32_t w0 = (mb & 1) ? kv.z : kv.x, w1 = (mb & 1) ? kv.w : kv.y;
       const float vk[4] = {bf16_lo(w0), bf16_hi(w0), bf16_lo(w1), bf16_hi(w1)};
       float o[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) o[i] = (r > 0) ? mu * vk[i] + omu * (O[nb][mb][i] * inv) : vk[i];
+      for (int i = 0; i < 4; ++i) o[i] = (r > 0) ? mu * vk[i] + omu * (st.O[nb][mb][i] * inv) : vk[i];
       const int64_t off = orow_j * D + mb * 16 + 4 * lg;
-      if (p.v_fp32)
+      if (VFP32)
         st16(reinterpret_cast<float *>(vout) + off,
              u32x4{__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]), __float_as_uint(o[3])});
       else
@@ -284,16 +382,21 @@ __global__ __launch_bounds__(256, 2) void k_fuse(PrunePlan p) {
   }
 }
 
+template <int D>
+hipError_t launch_fuse_d(const PrunePlan &p, hipStream_t st, uint32_t grid) {
+  if (p.v_fp32)
+    hipLaunchKernelGGL((k_fuse<D, true>), dim3(grid), dim3(256), 0, st, p);
+  else
+    hipLaunchKernelGGL((k_fuse<D, false>), dim3(grid), dim3(256), 0, st, p);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_fuse(const PrunePlan &p, hipStream_t st) {
-  const uint32_t grid = (uint32_t)p.h * p.B * p.Hkv * p.nfuse;
-  if (grid == 0) return hipSuccess;
-  if (p.d == 128)
-    hipLaunchKernelGGL(k_fuse<128>, dim3(grid), dim3(256), 0, st, p);
-  else
-    hipLaunchKernelGGL(k_fuse<64>, dim3(grid), dim3(256), 0, st, p);
-  return hipGetLastError();
+  if (p.nfunits == 0) return hipSuccess;
+  const uint32_t grid = (uint32_t)kXcds * (uint32_t)((p.nfunits + kXcds - 1) / kXcds) * (uint32_t)p.nfuse;
+  return p.d == 128 ? launch_fuse_d<128>(p, st, grid) : launch_fuse_d<64>(p, st, grid);
 }
 
 }  // namespace vc

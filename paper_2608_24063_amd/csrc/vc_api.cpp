@@ -25,11 +25,12 @@ struct Layout {
   int32_t nqg, nks, ncol, nfuse, nmax;
   int64_t Ntot;
   std::vector<int32_t> n, k, ns;       // n[B], k[B*L], ns[B*L]
+  std::vector<int32_t> funit;          // fusion units, longest drop list first
   std::vector<int64_t> toff, orow, drow;
   // workspace regions (byte offsets)
   size_t off_plan, plan_bytes, off_qbf, off_part, off_S, off_gs, off_drop, total;
   // offsets inside the plan blob
-  size_t p_lp, p_nb, p_toff, p_kk, p_ns, p_orow, p_drow;
+  size_t p_lp, p_nb, p_toff, p_kk, p_ns, p_orow, p_drow, p_funit;
 };
 
 vc_status check_shape(const vc_shape *s) {
@@ -104,6 +105,20 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   y.nks = (int32_t)std::max<int64_t>(1, nks);
   y.ncol = std::max(1, (y.nmax + kColKeys - 1) / kColKeys);
   y.nfuse = std::max(1, (kmax + kFuseRows - 1) / kFuseRows);
+  // Fusion units (layer < h with kept rows), ordered by dropped-row count,
+  // descending: every workgroup of a unit walks all of its dropped tiles, so
+  // dispatching the longest chains first bounds the tail.
+  y.funit.clear();
+  for (int32_t l = 0; l < y.h; ++l)
+    for (int32_t b = 0; b < y.B; ++b)
+      if (y.k[(size_t)b * y.L + l] > 0)
+        for (int32_t g = 0; g < y.Hkv; ++g) y.funit.push_back((l * y.B + b) * y.Hkv + g);
+  auto drops = [&](int32_t u) {
+    const int32_t l = u / (y.Hkv * y.B), b = (u / y.Hkv) % y.B;
+    return y.ns[(size_t)b * y.L + l] - y.k[(size_t)b * y.L + l];
+  };
+  std::stable_sort(y.funit.begin(), y.funit.end(),
+                   [&](int32_t a, int32_t c) { return drops(a) > drops(c); });
 
   // Plan blob.
   size_t o = 0;
@@ -114,6 +129,7 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   y.p_nb = o; o += sizeof(int32_t) * y.B;
   y.p_kk = o; o += sizeof(int32_t) * y.B * y.L;
   y.p_ns = o; o += sizeof(int32_t) * y.B * y.L;
+  y.p_funit = o; o += sizeof(int32_t) * y.funit.size();
   o = (o + 7) & ~size_t(7);
   y.plan_bytes = o;
 
@@ -234,11 +250,13 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   std::memcpy(blob.data() + y.p_nb, y.n.data(), sizeof(int32_t) * y.n.size());
   std::memcpy(blob.data() + y.p_kk, y.k.data(), sizeof(int32_t) * y.k.size());
   std::memcpy(blob.data() + y.p_ns, y.ns.data(), sizeof(int32_t) * y.ns.size());
+  if (!y.funit.empty()) std::memcpy(blob.data() + y.p_funit, y.funit.data(), sizeof(int32_t) * y.funit.size());
 
   PrunePlan pl{};
   pl.B = y.B; pl.L = y.L; pl.Hq = y.Hq; pl.Hkv = y.Hkv; pl.d = y.d; pl.W = y.W; pl.G = y.G;
   pl.R = y.R; pl.h = y.h; pl.Ls = y.Ls; pl.mode = y.mode; pl.v_fp32 = y.vfp32;
   pl.nqg = y.nqg; pl.nks = y.nks; pl.ncol = y.ncol; pl.nfuse = y.nfuse; pl.nmax = y.nmax;
+  pl.nfunits = (int32_t)y.funit.size();
   pl.sc = (float)(1.4426950408889634 / std::sqrt((double)y.d));
   pl.tc = (float)(1.4426950408889634 / (double)params->tau);
   pl.mu = params->mu;
@@ -251,6 +269,7 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   pl.ns = reinterpret_cast<const int32_t *>(pb + y.p_ns);
   pl.orow = reinterpret_cast<const int64_t *>(pb + y.p_orow);
   pl.drow = reinterpret_cast<const int64_t *>(pb + y.p_drow);
+  pl.funit = reinterpret_cast<const int32_t *>(pb + y.p_funit);
   pl.qbf = reinterpret_cast<uint16_t *>(ws + y.off_qbf);
   pl.part = reinterpret_cast<float2 *>(ws + y.off_part);
   pl.rowst = nullptr;

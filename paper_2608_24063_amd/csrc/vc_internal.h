@@ -31,6 +31,7 @@ struct PrunePlan {
   int32_t nqg, nks;   // stats grid: query groups x key splits per unit
   int32_t ncol;       // column-sum chunks per unit (max over sequences)
   int32_t nfuse;      // fusion tiles per unit (max over units)
+  int32_t nfunits;    // units with kept rows (fusion grid = 8 x ceil(nfunits/8) x nfuse)
   int32_t nmax;       // max n_b
   float sc;           // log2(e) / sqrt(d)
   float tc;           // log2(e) / tau
@@ -43,6 +44,7 @@ struct PrunePlan {
   const int32_t *ns;    // [B*L] survivors per (b, l)
   const int64_t *orow;  // [L*(B+1)] output row offsets per layer
   const int64_t *drow;  // [L*(B+1)] dropped-row offsets per layer
+  const int32_t *funit; // [nfunits] fusion units, most dropped rows first
   uint16_t *qbf;        // [Ls][B][Hq][W][d] window queries in bf16
   float2 *part;         // [U][nks][R] partial row statistics (max*sc, sum)
   float2 *rowst;        // [U][R] row statistics (max*sc, 1/sum)
