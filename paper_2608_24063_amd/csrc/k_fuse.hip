@@ -35,18 +35,17 @@ constexpr float kNegInf = -__builtin_inff();
 // raised (and the accumulators rescaled); fp32 has ample range for that.
 constexpr float kSlack = 8.f;
 
-// Row pitch of the staged dropped tile: 32 bytes of padding.  Measured on
-// gfx950, this keeps the transposing reads conflict-free and costs the direct
-// 8-byte reads one extra cycle in three; a single row-major copy serves both.
+// Staged dropped tile: rows of D bf16 at a pitch of D + 16 elements.  On
+// gfx950 (LDS serves 64 banks x 4 bytes per pass) this pitch keeps all three
+// access patterns below conflict-free at full rate (measured): 16-byte writes
+// of one row per 16 lanes, 16-byte reads of 16 rows x 4 chunks (the S^T A
+// operand), and transposing 8-byte reads of 4 rows x 32 bytes per 16 lanes
+// (the O^T A operand).
 template <int D>
 constexpr int kPitchRow = D + 16;
 
-// 8 bf16 at d = {c..c+3, c+16..c+19} of one staged row: the k-element order
-// shared by both operands of S^T for lane group lg at k-step s (c = 32 s + 4 lg).
-__device__ __forceinline__ bf16x8 load_split8_lds(const uint16_t *row, int c) {
-  const u32x2 a = *reinterpret_cast<const u32x2 *>(row + c);
-  const u32x2 b = *reinterpret_cast<const u32x2 *>(row + c + 16);
-  return as_bf16x8(u32x4{a.x, a.y, b.x, b.y});
+__device__ __forceinline__ bf16x8 lds16(const uint16_t *p) {
+  return as_bf16x8(*reinterpret_cast<const u32x4 *>(p));
 }
 
 // gfx950 transposing LDS read: within each group of 16 lanes, lane 4a+b gets
@@ -58,36 +57,29 @@ __device__ __forceinline__ u32x2 lds_read_tr16(const uint16_t *p) {
 }
 
 // Rows of one 64-row dropped tile between their global load and their LDS
-// store: thread t owns rows 2*(t%32) and 2*(t%32)+1 and the 16-byte chunks
-// (t/32) + 8*it of both.  Row indices are valid (clamped) token indices.
+// store: thread t owns 16-byte chunk t % kCpr of rows t / kCpr + kRpp * it,
+// so every 16 lanes move whole rows (coalesced in HBM, conflict-free in LDS).
 template <int D>
 struct DropRegs {
-  static constexpr int kIt = D / 64;
-  u32x4 a[kIt], b[kIt];
-  __device__ __forceinline__ void load(const uint16_t *V, int ia, int ib, int c0) {
+  static constexpr int kCpr = D / 8;             // 16-byte chunks per row
+  static constexpr int kRpp = 256 / kCpr;        // rows per pass of the block
+  static constexpr int kIt = kDropTile / kRpp;   // rows per thread
+  u32x4 v[kIt];
+  __device__ __forceinline__ void load(const uint16_t *V, const int (&row)[kIt], int chunk) {
 #pragma unroll
-    for (int it = 0; it < kIt; ++it) {
-      const int c = c0 + 8 * it;
-      a[it] = ld16(V + (int64_t)ia * D + c * 8);
-      b[it] = ld16(V + (int64_t)ib * D + c * 8);
-    }
+    for (int it = 0; it < kIt; ++it) v[it] = ld16(V + (int64_t)row[it] * D + chunk * 8);
   }
-  __device__ __forceinline__ void store(uint16_t *vr, int pp, int c0) const {
+  __device__ __forceinline__ void store(uint16_t *vr, int row0, int chunk) const {
     constexpr int PR = kPitchRow<D>;
-    const int ra = 2 * pp;
 #pragma unroll
-    for (int it = 0; it < kIt; ++it) {
-      const int c = c0 + 8 * it;
-      *reinterpret_cast<u32x4 *>(vr + ra * PR + c * 8) = a[it];
-      *reinterpret_cast<u32x4 *>(vr + (ra + 1) * PR + c * 8) = b[it];
-    }
+    for (int it = 0; it < kIt; ++it) *reinterpret_cast<u32x4 *>(vr + (row0 + kRpp * it) * PR + chunk * 8) = v[it];
   }
 };
 
 template <int D>
 struct FuseState {
   static constexpr int KS = D / 32, MB = D / 16, NB = 2;
-  bf16x8 bvk[NB][KS];  // kept values, B operand of S^T
+  bf16x8 bvk[NB][KS];  // kept values, B operand of S^T (elements 32 s + 8 lg ..)
   f32x4 O[NB][MB];     // O^T accumulators
   float mrow[NB];      // running max of the scaled logits (x log2(e)/tau)
   float lsum[NB];      // this lane's share of the running denominator
@@ -103,14 +95,15 @@ __device__ __forceinline__ void fuse_tile(FuseState<D> &st, const uint16_t *vt, 
   // S^T = V_d V_k^T for 64 dropped x 32 kept rows; A operands one k-step ahead.
   f32x4 acc[NB][4];
   bf16x8 a[2][4];
+  // k-step s, lane group lg: elements 32 s + 8 lg .. + 7 of the row.
 #pragma unroll
-  for (int db = 0; db < 4; ++db) a[0][db] = load_split8_lds(vt + (db * 16 + lr) * PR, 4 * lg);
+  for (int db = 0; db < 4; ++db) a[0][db] = lds16(vt + (db * 16 + lr) * PR + 8 * lg);
 #pragma unroll
   for (int s = 0; s < KS; ++s) {
     if (s + 1 < KS) {
 #pragma unroll
       for (int db = 0; db < 4; ++db)
-        a[(s + 1) & 1][db] = load_split8_lds(vt + (db * 16 + lr) * PR, 32 * (s + 1) + 4 * lg);
+        a[(s + 1) & 1][db] = lds16(vt + (db * 16 + lr) * PR + 32 * (s + 1) + 8 * lg);
     }
 #pragma unroll
     for (int db = 0; db < 4; ++db)
@@ -222,96 +215,116 @@ __device__ __forceinline__ void fuse_tile(FuseState<D> &st, const uint16_t *vt, 
 // two matrix instructions.
 template <int D, bool VFP32>
 __global__ __launch_bounds__(256, 2) void k_fuse(PrunePlan p) {
-  constexpr int KS = D / 32, MB = D / 16, NB = 2, PR = kPitchRow<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t vr[2][kDropTile * PR];
-  __shared__ int32_t kidx[kFuseRows];
+  constexpr int KS = D / 32, MB = D / 16, NB = 2;
+  __shared__ __attribute__((aligned(16))) uint16_t vr[2][kDropTile * kPitchRow<D>];
 
-  // Block -> (unit, tile): block x*... runs on XCD blockIdx % 8; each XCD
-  // takes every 8th unit of the longest-first list, all tiles of a unit on
-  // the same XCD (they share the unit's dropped rows in L2).
+  // Block -> (unit, tile): block b runs on XCD b % 8; each XCD takes every
+  // 8th unit of the longest-first list, all tiles of a unit on the same XCD
+  // (they share the unit's dropped rows in L2).
   const uint32_t x = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
   const int rank = (int)(x + kXcds * (slot / p.nfuse));
   const int tile = (int)(slot % p.nfuse);
   if (rank >= p.nfunits) return;
-  const int u = ldg(p.funit + rank);
-  const int g = u % p.Hkv;
-  const int b = (u / p.Hkv) % p.B;
-  const int l = u / (p.Hkv * p.B);
-  const int k = ldg(p.kk + b * p.L + l);
+  const u32x4 *rec = reinterpret_cast<const u32x4 *>(p.funit + rank);
+  const u32x4 r0 = ld16(rec), r1 = ld16(rec + 1), r2 = ld16(rec + 2), r3 = ld16(rec + 3);
+  auto ptr = [](uint32_t lo, uint32_t hi) { return (uint64_t)lo | ((uint64_t)hi << 32); };
+  const int k = (int)r3.x, r = (int)r3.y, n = (int)r3.z;
   const int j0 = tile * kFuseRows;
   if (j0 >= k) return;
-  const int n = ldg(p.nb + b);
-  const int r = ldg(p.ns + b * p.L + l) - k;
+  const uint16_t *Kin = reinterpret_cast<const uint16_t *>(ptr(r0.x, r0.y));
+  const uint16_t *Vin = reinterpret_cast<const uint16_t *>(ptr(r0.z, r0.w));
+  uint16_t *Kout = reinterpret_cast<uint16_t *>(ptr(r1.x, r1.y)) + (int64_t)j0 * D;
+  void *vout = reinterpret_cast<void *>(ptr(r1.z, r1.w));
+  const int32_t *kept = reinterpret_cast<const int32_t *>(ptr(r2.x, r2.y)) + j0;
+  const int32_t *drop = reinterpret_cast<const int32_t *>(ptr(r2.z, r2.w));
   const int nrows = min(kFuseRows, k - j0);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
 
-  const int64_t orow = ldg(p.orow + l * (p.B + 1) + b) + (int64_t)g * k;
-  const int32_t *idx = reinterpret_cast<const int32_t *>(ldg(p.lp + LP_IDX * p.L + l)) + orow;
-  const int32_t *drop = reinterpret_cast<const int32_t *>(ldg(p.lp + LP_DROP * p.L + l)) +
-                        ldg(p.drow + l * (p.B + 1) + b) + (int64_t)g * r;
-  const int64_t ioff = (ldg(p.toff + b) * p.Hkv + (int64_t)g * n) * D;
-  const uint16_t *Kin = reinterpret_cast<const uint16_t *>(ldg(p.lp + LP_K_IN * p.L + l)) + ioff;
-  const uint16_t *Vin = reinterpret_cast<const uint16_t *>(ldg(p.lp + LP_V_IN * p.L + l)) + ioff;
-  uint16_t *Kout = reinterpret_cast<uint16_t *>(ldg(p.lp + LP_K_OUT * p.L + l)) + orow * D;
-
   // Token indices come from the selection kernel; clamping keeps every
   // gathered row inside the unit even if they were corrupted.
   auto clampi = [&](int v) { return min(max(v, 0), n - 1); };
-  if (tid < nrows) kidx[tid] = clampi(ldg(idx + j0 + tid));
+  auto kept_idx = [&](int row) { return ldg(kept + min(row, nrows - 1)); };
 
-  // Dropped-tile pipeline.  Indices are read raw and clamped one tile later,
-  // so no wait on them lands right behind the row loads.  Tiles past the end
-  // re-read the last tile (harmless, never consumed).
+  // Every index this thread needs before the first tile, in one batch:
+  // kept rows of its key-copy chunks and of its lanes' value operands, and
+  // dropped rows of tiles 0..3.  Dropped indices are read raw and clamped
+  // one tile later, so no wait on them lands right behind the row loads;
+  // tiles past the end re-read the last tile (never consumed).
+  constexpr int kCpr = D / 8;                          // 16-byte chunks per row
+  constexpr int kChunks = kFuseRows * kCpr / 256;      // key-copy chunks per thread
+  int kc_idx[kChunks];
+#pragma unroll
+  for (int i = 0; i < kChunks; ++i) kc_idx[i] = kept_idx((tid + 256 * i) / kCpr);
+  int kv_idx[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) kv_idx[nb] = kept_idx(w * 32 + nb * 16 + lr);
   const int ntiles = (r + kDropTile - 1) / kDropTile;
-  const int pp = tid & 31, c0 = tid >> 5;
-  auto raw_idx = [&](int dt, int row) -> int {
-    const int j = min(min(dt, ntiles - 1) * kDropTile + row, r - 1);
-    return ldg(drop + j);
+  using Regs = DropRegs<D>;
+  constexpr int kIt = Regs::kIt;
+  const int row0 = tid / Regs::kCpr, chunk = tid % Regs::kCpr;
+  auto raw_idx = [&](int dt, int (&o)[kIt]) {
+    const int base = min(dt, ntiles - 1) * kDropTile + row0;
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) o[it] = ldg(drop + min(base + Regs::kRpp * it, r - 1));
   };
-  DropRegs<D> set0, set1;
-  int pa = 0, pb = 0;  // raw indices of the next tile to load
+  auto clamp_rows = [&](const int (&in)[kIt], int (&o)[kIt]) {
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) o[it] = clampi(in[it]);
+  };
+  int di[4][kIt];
   if (ntiles > 0) {
-    const int a0 = raw_idx(0, 2 * pp), b0 = raw_idx(0, 2 * pp + 1);
-    const int a1 = raw_idx(1, 2 * pp), b1 = raw_idx(1, 2 * pp + 1);
-    const int a2 = raw_idx(2, 2 * pp), b2 = raw_idx(2, 2 * pp + 1);
-    pa = raw_idx(3, 2 * pp);
-    pb = raw_idx(3, 2 * pp + 1);
-    set0.load(Vin, clampi(a0), clampi(b0), c0);
-    set1.load(Vin, clampi(a1), clampi(b1), c0);
-    set0.store(vr[0], pp, c0);
-    set0.load(Vin, clampi(a2), clampi(b2), c0);
-  }
-  __syncthreads();
-
-  // Key pruning: bit copies of the kept rows (loads first, then stores).
-  {
-    constexpr int kChunks = kFuseRows * (D / 8) / 256;
-    u32x4 kc[kChunks];
 #pragma unroll
-    for (int i = 0; i < kChunks; ++i) {
-      const int c = tid + 256 * i, row = c / (D / 8), col = c % (D / 8);
-      kc[i] = ld16(Kin + (int64_t)kidx[row < nrows ? row : 0] * D + col * 8);
-    }
-#pragma unroll
-    for (int i = 0; i < kChunks; ++i) {
-      const int c = tid + 256 * i, row = c / (D / 8), col = c % (D / 8);
-      if (row < nrows) st16(Kout + (int64_t)(j0 + row) * D + col * 8, kc[i]);
-    }
+    for (int t = 0; t < 4; ++t) raw_idx(t, di[t]);
   }
 
+  // Row loads: key copies, kept values, dropped tiles 0 and 1.
+  u32x4 kc[kChunks];
+#pragma unroll
+  for (int i = 0; i < kChunks; ++i) kc[i] = ld16(Kin + (int64_t)clampi(kc_idx[i]) * D + ((tid + 256 * i) % kCpr) * 8);
   FuseState<D> st;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+    for (int s = 0; s < KS; ++s) st.bvk[nb][s] = as_bf16x8(ld16(Vin + (int64_t)clampi(kv_idx[nb]) * D + 32 * s + 8 * lg));
+  }
+  Regs set0, set1;
+  int pend[kIt];  // raw indices of the next tile to load
+  if (ntiles > 0) {
+    int rr[kIt];
+    clamp_rows(di[0], rr);
+    set0.load(Vin, rr, chunk);
+    clamp_rows(di[1], rr);
+    set1.load(Vin, rr, chunk);
+  }
+
+  // Key pruning: bit copies of the kept rows.
+#pragma unroll
+  for (int i = 0; i < kChunks; ++i) {
+    const int c = tid + 256 * i;
+    if (c / kCpr < nrows) st16(Kout + (int64_t)(c / kCpr) * D + (c % kCpr) * 8, kc[i]);
+  }
+  if (ntiles > 0) {
+    set0.store(vr[0], row0, chunk);
+    int rr[kIt];
+    clamp_rows(di[2], rr);
+    set0.load(Vin, rr, chunk);
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) pend[it] = di[3][it];
+  }
   bool kvalid[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    const int krow = w * 32 + nb * 16 + lr;
-    kvalid[nb] = krow < nrows;
+    kvalid[nb] = w * 32 + nb * 16 + lr < nrows;
+    if (!kvalid[nb]) {
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      const uint16_t *row = Vin + (int64_t)kidx[kvalid[nb] ? krow : 0] * D + 32 * s + 4 * lg;
-      const u32x2 x0 = ld8(row), y0 = ld8(row + 16);
-      st.bvk[nb][s] = kvalid[nb] ? as_bf16x8(u32x4{x0.x, x0.y, y0.x, y0.y}) : as_bf16x8(u32x4{0, 0, 0, 0});
+      for (int s = 0; s < KS; ++s) st.bvk[nb][s] = as_bf16x8(u32x4{0, 0, 0, 0});
     }
+  }
+  __syncthreads();
+
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) st.O[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
     // Running maxima are pre-multiplied by log2(e)/tau; the finite floor makes
@@ -326,12 +339,14 @@ __global__ __launch_bounds__(256, 2) void k_fuse(PrunePlan p) {
   // tile t+4, and synchronise.
   auto advance = [&](auto par, int t) {
     constexpr int PAR = decltype(par)::value;
-    DropRegs<D> &nx = PAR ? set0 : set1;
-    nx.store(vr[PAR ^ 1], pp, c0);
-    const int na = raw_idx(t + 4, 2 * pp), nb2 = raw_idx(t + 4, 2 * pp + 1);
-    nx.load(Vin, clampi(pa), clampi(pb), c0);
-    pa = na;
-    pb = nb2;
+    Regs &nx = PAR ? set0 : set1;
+    nx.store(vr[PAR ^ 1], row0, chunk);
+    int nxt[kIt], rr[kIt];
+    raw_idx(t + 4, nxt);
+    clamp_rows(pend, rr);
+    nx.load(Vin, rr, chunk);
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) pend[it] = nxt[it];
     __syncthreads();
   };
   using P0 = std::integral_constant<int, 0>;
@@ -355,7 +370,6 @@ __global__ __launch_bounds__(256, 2) void k_fuse(PrunePlan p) {
   }
 
   const float mu = p.mu, omu = 1.f - p.mu;
-  void *vout = reinterpret_cast<void *>(ldg(p.lp + LP_V_OUT * p.L + l));
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     float ls = st.lsum[nb];
@@ -363,11 +377,15 @@ __global__ __launch_bounds__(256, 2) void k_fuse(PrunePlan p) {
     ls += shfl_xor(ls, 32);
     if (!kvalid[nb]) continue;
     const float inv = (r > 0 && ls > 0.f) ? 1.f / ls : 0.f;
-    const int64_t orow_j = orow + j0 + w * 32 + nb * 16 + lr;
+    const int64_t orow_j = j0 + w * 32 + nb * 16 + lr;
+    // Kept values at this lane's output columns 16 mb + 4 lg + i (L2-hot).
+    const uint16_t *vrow = Vin + (int64_t)clampi(kv_idx[nb]) * D + 4 * lg;
+    u32x2 kvv[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) kvv[mb] = ld8(vrow + 16 * mb);
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
-      const u32x4 kv = as_u32x4(st.bvk[nb][mb / 2]);
-      const uint32_t w0 = (mb & 1) ? kv.z : kv.x, w1 = (mb & 1) ? kv.w : kv.y;
+      const uint32_t w0 = kvv[mb].x, w1 = kvv[mb].y;
       const float vk[4] = {bf16_lo(w0), bf16_hi(w0), bf16_lo(w1), bf16_hi(w1)};
       float o[4];
 #pragma unroll

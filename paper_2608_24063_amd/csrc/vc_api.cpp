@@ -129,7 +129,8 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   y.p_nb = o; o += sizeof(int32_t) * y.B;
   y.p_kk = o; o += sizeof(int32_t) * y.B * y.L;
   y.p_ns = o; o += sizeof(int32_t) * y.B * y.L;
-  y.p_funit = o; o += sizeof(int32_t) * y.funit.size();
+  o = (o + 15) & ~size_t(15);
+  y.p_funit = o; o += sizeof(FuseUnit) * y.funit.size();
   o = (o + 7) & ~size_t(7);
   y.plan_bytes = o;
 
@@ -250,7 +251,32 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   std::memcpy(blob.data() + y.p_nb, y.n.data(), sizeof(int32_t) * y.n.size());
   std::memcpy(blob.data() + y.p_kk, y.k.data(), sizeof(int32_t) * y.k.size());
   std::memcpy(blob.data() + y.p_ns, y.ns.data(), sizeof(int32_t) * y.ns.size());
-  if (!y.funit.empty()) std::memcpy(blob.data() + y.p_funit, y.funit.data(), sizeof(int32_t) * y.funit.size());
+  {
+    // Fusion unit records: absolute row addresses, so the fusion kernel
+    // needs one dependent load before its index loads.
+    FuseUnit *fr = reinterpret_cast<FuseUnit *>(blob.data() + y.p_funit);
+    const size_t vsz = y.vfp32 ? 4 : 2;
+    for (size_t i = 0; i < y.funit.size(); ++i) {
+      const int32_t u = y.funit[i];
+      const int32_t g = u % y.Hkv, b = (u / y.Hkv) % y.B, l = u / (y.Hkv * y.B);
+      const int32_t kk = y.k[(size_t)b * y.L + l], nn = y.n[b];
+      const int32_t rr = y.ns[(size_t)b * y.L + l] - kk;
+      const int64_t in_row = y.toff[b] * y.Hkv + (int64_t)g * nn;
+      const int64_t out_row = y.orow[(size_t)l * (y.B + 1) + b] + (int64_t)g * kk;
+      const int64_t drop_row = y.drow[(size_t)l * (y.B + 1) + b] + (int64_t)g * rr;
+      FuseUnit f{};
+      f.k_in = lp[LP_K_IN * y.L + l] + (uint64_t)(in_row * y.d * 2);
+      f.v_in = lp[LP_V_IN * y.L + l] + (uint64_t)(in_row * y.d * 2);
+      f.k_out = lp[LP_K_OUT * y.L + l] + (uint64_t)(out_row * y.d * 2);
+      f.v_out = lp[LP_V_OUT * y.L + l] + (uint64_t)(out_row * y.d * vsz);
+      f.kept = lp[LP_IDX * y.L + l] + (uint64_t)(out_row * 4);
+      f.drop = lp[LP_DROP * y.L + l] + (uint64_t)(drop_row * 4);
+      f.k = kk;
+      f.r = rr;
+      f.n = nn;
+      fr[i] = f;
+    }
+  }
 
   PrunePlan pl{};
   pl.B = y.B; pl.L = y.L; pl.Hq = y.Hq; pl.Hkv = y.Hkv; pl.d = y.d; pl.W = y.W; pl.G = y.G;
@@ -269,7 +295,7 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   pl.ns = reinterpret_cast<const int32_t *>(pb + y.p_ns);
   pl.orow = reinterpret_cast<const int64_t *>(pb + y.p_orow);
   pl.drow = reinterpret_cast<const int64_t *>(pb + y.p_drow);
-  pl.funit = reinterpret_cast<const int32_t *>(pb + y.p_funit);
+  pl.funit = reinterpret_cast<const FuseUnit *>(pb + y.p_funit);
   pl.qbf = reinterpret_cast<uint16_t *>(ws + y.off_qbf);
   pl.part = reinterpret_cast<float2 *>(ws + y.off_part);
   pl.rowst = nullptr;

@@ -20,6 +20,16 @@ constexpr int kSelectThreads = 512;
 constexpr int kSelectPerThread = 64;  // => n <= 32768 tokens per sequence
 constexpr int kMaxTokens = kSelectThreads * kSelectPerThread;
 
+// One fusion unit (layer, sequence, kv head) with kept rows, as the fusion
+// kernel reads it: absolute addresses of the unit's first rows and its sizes.
+struct FuseUnit {
+  uint64_t k_in, v_in;     // bf16 [n][d] input keys / values of the unit
+  uint64_t k_out, v_out;   // bf16 [k][d] pruned keys; bf16 or fp32 [k][d] fused values
+  uint64_t kept, drop;     // int32 [k] kept / [r] dropped token indices
+  int32_t k, r, n, pad;
+};
+static_assert(sizeof(FuseUnit) == 64, "fusion unit record is four 16-byte words");
+
 // Everything the prune kernels need, by value (a few hundred bytes).  Array
 // members point into the device workspace, filled by the plan upload kernel.
 struct PrunePlan {
@@ -44,7 +54,7 @@ struct PrunePlan {
   const int32_t *ns;    // [B*L] survivors per (b, l)
   const int64_t *orow;  // [L*(B+1)] output row offsets per layer
   const int64_t *drow;  // [L*(B+1)] dropped-row offsets per layer
-  const int32_t *funit; // [nfunits] fusion units, most dropped rows first
+  const FuseUnit *funit; // [nfunits] fusion units, most dropped rows first
   uint16_t *qbf;        // [Ls][B][Hq][W][d] window queries in bf16
   float2 *part;         // [U][nks][R] partial row statistics (max*sc, sum)
   float2 *rowst;        // [U][R] row statistics (max*sc, 1/sum)
