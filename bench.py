@@ -43,7 +43,14 @@ def parse():
     ap.add_argument("--no-flush", action="store_true", help="keep caches warm between steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
-    ap.add_argument("--cpu-units", type=int, default=48, help="oracle units in the CPU sample")
+    ap.add_argument("--cpu-units", type=int, default=0,
+                    help="oracle units in the CPU sample (0: every unit of the workload)")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run a plain device copy of known size (HBM counter calibration)")
+    ap.add_argument("--reduce-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="reduce two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this script "
+                         "into the traffic summary under profiles/, then exit")
+    ap.add_argument("--pmc-command", default="", help="command line recorded in the traffic summary")
     return ap.parse_args()
 
 
@@ -74,22 +81,164 @@ def algorithmic(w, pc, n_list):
     return out
 
 
+# Kernel of each timed stage, and the sources its code comes from (the hash of
+# these files decides whether stored HBM counters still describe the kernel).
+STAGE_KERNEL = {
+    "score_stats": ("k_score_stats", ["k_score.hip"]),
+    "score_colsum": ("k_score_colsum", ["k_score.hip"]),
+    "select": ("k_select", ["k_select.hip"]),
+    "gather_fuse": ("k_fuse", ["k_fuse.hip"]),
+}
+COPY_PROBE_BYTES = 1 << 30
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_vllm7b_hbm_counters.md")
+
+
+def kernel_hash(files):
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_24063_amd", "csrc")
+    for f in sorted(set(files + ["vc_device.h", "vc_internal.h"])):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def copy_probe(torch, dev):
+    """A plain device-to-device copy of COPY_PROBE_BYTES: it reads and writes
+    exactly that many bytes of HBM, which calibrates FETCH_SIZE / WRITE_SIZE."""
+    src = torch.ones(COPY_PROBE_BYTES // 4, dtype=torch.int32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
+def reduce_pmc(fetch_dir, write_dir, command):
+    """Per-dispatch HBM bytes of each prune kernel from two counter runs,
+    scaled by what the same counters read for the copy probe."""
+    import csv
+    import glob
+    import re
+
+    def load(d, counter):
+        per = {}
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for row in csv.DictReader(open(f)):
+                if row["Counter_Name"] != counter:
+                    continue
+                name = row["Kernel_Name"]
+                m = re.search(r"(k_\w+)<", name) or re.search(r"(k_\w+)\(", name)
+                # the copy probe is the runtime's device-to-device blit
+                key = m.group(1) if (m and "vc::" in name) else ("copy" if "copyBuffer" in name else None)
+                if key is None:
+                    continue
+                per.setdefault(key, []).append((float(row["Counter_Value"]), int(row["Grid_Size"])))
+        return per
+
+    fetch, write = load(fetch_dir, "FETCH_SIZE"), load(write_dir, "WRITE_SIZE")
+    # The copy probe: the copy dispatch with the largest counter value.
+    fc = max(v for v, _ in fetch.get("copy", [(0.0, 0)]))
+    wc = max(v for v, _ in write.get("copy", [(0.0, 0)]))
+    if fc <= 0 or wc <= 0:
+        raise SystemExit("no copy-probe dispatch found in the counter runs (run bench.py --copy-probe)")
+    sf, sw = COPY_PROBE_BYTES / (fc * 1024.0), COPY_PROBE_BYTES / (wc * 1024.0)
+    rec = {"copy_probe_bytes": COPY_PROBE_BYTES, "fetch_kib_copy": fc, "write_kib_copy": wc,
+           "fetch_scale": sf, "write_scale": sw, "kernels": {}}
+    for stage, (kname, files) in STAGE_KERNEL.items():
+        if kname not in fetch or kname not in write:
+            continue
+        fk = sum(v for v, _ in fetch[kname]) / len(fetch[kname])
+        wk = sum(v for v, _ in write[kname]) / len(write[kname])
+        rec["kernels"][stage] = {"kernel": kname, "fetch_kib": fk, "write_kib": wk,
+                                 "hbm_bytes": fk * 1024.0 * sf + wk * 1024.0 * sw,
+                                 "source_hash": kernel_hash(files)}
+    lines = ["# HBM traffic per dispatch, 7B-shaped workload (rocprofv3 FETCH_SIZE / WRITE_SIZE)", "",
+             "Command (each counter in its own run):", "", "```", command or "(not recorded)", "```", "",
+             f"Copy probe: {COPY_PROBE_BYTES} bytes read and written; FETCH_SIZE read {fc:.0f} KiB "
+             f"(scale {sf:.4f}), WRITE_SIZE read {wc:.0f} KiB (scale {sw:.4f}).", "",
+             "| stage | kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled HBM MB |", "|---|---|---|---|---|"]
+    for stage, k in rec["kernels"].items():
+        lines.append(f"| {stage} | {k['kernel']} | {k['fetch_kib']:.0f} | {k['write_kib']:.0f} | "
+                     f"{k['hbm_bytes'] / 1e6:.1f} |")
+    lines += ["", "Machine-readable (read by bench.py):", "", "```json", json.dumps(rec), "```", ""]
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as f:
+        f.write("\n".join(lines))
+    print("\n".join(lines))
+
+
+def stored_traffic(stage):
+    """Scaled HBM bytes per dispatch of a stage's kernel, if the stored counters
+    were taken on the current source; else None."""
+    try:
+        text = open(TRAFFIC_FILE).read()
+        blob = text.split("```json", 1)[1].split("```", 1)[0]
+        rec = json.loads(blob)["kernels"].get(stage)
+    except (OSError, IndexError, ValueError, KeyError):
+        return None
+    if not rec or rec.get("source_hash") != kernel_hash(STAGE_KERNEL[stage][1]):
+        return None
+    return rec["hbm_bytes"]
+
+
+class HipEvents:
+    """Timing events without the system-scope release fence (HIP's
+    hipEventDisableSystemFence), so bracketing each stage costs little."""
+    FLAGS = 0x20000000  # hipEventDisableSystemFence
+
+    def __init__(self, count):
+        import ctypes
+        self.ct = ctypes
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.ev = []
+        for _ in range(count):
+            h = ctypes.c_void_p()
+            if self.hip.hipEventCreateWithFlags(ctypes.byref(h), self.FLAGS) != 0:
+                raise RuntimeError("hipEventCreateWithFlags failed")
+            self.ev.append(h.value)
+
+    def ms(self, a, b):
+        out = self.ct.c_float()
+        if self.hip.hipEventElapsedTime(self.ct.byref(out), self.ev[a], self.ev[b]) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return out.value
+
+    def close(self):
+        for h in self.ev:
+            self.hip.hipEventDestroy(h)
+
+
 def time_prune(pc, steps, warmup, flush_buf, torch):
+    """Whole-path time per step (two events per step, nothing between the
+    kernels), then per-stage times from separate steps bracketed stage by
+    stage.  Caches are flushed before every step, outside the timed region."""
     for _ in range(warmup):
         if flush_buf is not None:
             flush_buf.sum()
         pc.run()
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(steps)]
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(steps):
         if flush_buf is not None:
             flush_buf.sum()  # reading 1 GiB evicts L2 and the Infinity Cache; not timed
-        pc.run(events=ev[s])
+        ev[s][0].record()
+        pc.run()
+        ev[s][1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    tot = [e[0].elapsed_time(e[6]) for e in ev]
-    stage = [[e[i].elapsed_time(e[i + 1]) for i in range(6)] for e in ev]
+    tot = [a.elapsed_time(b) for a, b in ev]
+    hev = HipEvents(7 * steps)
+    for s in range(steps):
+        if flush_buf is not None:
+            flush_buf.sum()
+        pc.run(events=hev.ev[7 * s:7 * s + 7])
+    torch.cuda.synchronize()
+    stage = [[hev.ms(7 * s + i, 7 * s + i + 1) for i in range(6)] for s in range(steps)]
+    hev.close()
     return tot, stage, wall
 
 
@@ -182,6 +331,7 @@ def cpu_baseline(w, pc, host, units_wanted):
     for x in n:
         toff.append(toff[-1] + x)
     allu = [(l, b, g) for l in range(pc.h) for b in range(w.B) for g in range(Hkv)]
+    units_wanted = len(allu) if units_wanted <= 0 else min(units_wanted, len(allu))
     step = max(1, len(allu) // units_wanted)
     units = allu[::step][:units_wanted]
 
@@ -208,6 +358,9 @@ def cpu_baseline(w, pc, host, units_wanted):
 
 def main():
     args = parse()
+    if args.reduce_pmc:
+        reduce_pmc(args.reduce_pmc[0], args.reduce_pmc[1], args.pmc_command)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -235,7 +388,8 @@ def main():
                    [dv["V"][l] for l in range(w.L)], [dv["Q"][l] for l in range(w.L)])
     # Flush by reading (not writing) 1 GiB, so the caches hold clean lines and
     # the measured kernels pay no write-back of the flush data.
-    flush = None if args.no_flush else torch.ones(1 << 28, dtype=torch.int32, device=dev)
+    # (float32: a sum of int32 would be widened to int64 first, writing 2 GiB.)
+    flush = None if args.no_flush else torch.ones(1 << 28, dtype=torch.float32, device=dev)
     print(f"[bench] timing {args.steps} prune steps after {args.warmup} warm-up", file=sys.stderr, flush=True)
     tot, stage, wall = time_prune(pc, args.steps, args.warmup, flush, torch)
     ms = sum(tot) / len(tot)
@@ -252,13 +406,15 @@ def main():
     else:
         roof = dict(bound="hbm", achieved=a["bytes"] / t / 1e9, peak=HBM_PEAK_GBS, unit="GB/s")
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
+    roof["traffic"] = stored_traffic(dom)
     roof["kernel"] = dom
     roof["kernel_us"] = stage_us[dom]
     roof["hbm_frac"] = fr_hbm
     roof["mfma_frac"] = fr_mfma
     roof["exp_per_s"] = a["exps"] / t
 
+    if args.copy_probe:
+        copy_probe(torch, dev)
     dec = None
     if not args.no_decode:
         dsteps = args.decode_steps or w.decode_steps
@@ -266,7 +422,7 @@ def main():
         dec = decode_latency(w, pc, dev, dsteps, flush, torch, sg)
     cpu = None
     if not args.no_cpu_baseline:
-        print(f"[bench] CPU oracle sample ({args.cpu_units} units)", file=sys.stderr, flush=True)
+        print(f"[bench] CPU oracle ({args.cpu_units or 'all'} units)", file=sys.stderr, flush=True)
         cpu = cpu_baseline(w, pc, host, args.cpu_units)
 
     rec = {

@@ -1,7 +1,8 @@
 // k_setup.hip -- moves the host-built prune plan (layer pointer table, budgets,
-// offsets) into the device workspace.  The plan travels as kernel arguments,
-// at most kUploadBytes per launch, so no host buffer has to outlive the call
-// and nothing is copied through pageable memory.
+// offsets, fusion unit records) into the device workspace.  The plan travels
+// as kernel arguments, up to 30 KB per launch (one launch for the shapes seen
+// in practice), so no host buffer has to outlive the call and nothing is
+// copied through pageable memory.
 #include "vc_device.h"
 #include "vc_internal.h"
 
@@ -9,16 +10,32 @@ namespace vc {
 
 namespace {
 
-constexpr int kUploadWords = 480;  // 1920-byte payload per launch
+// Payload sizes: the launch copies the whole argument block, so the smallest
+// one that holds the plan is used.
+constexpr uint32_t kSmallWords = 480, kMidWords = 2040, kBigWords = 7680;  // 1.9 / 8 / 30 KB
 
+template <uint32_t W>
 struct UploadChunk {
   uint32_t words;
   uint32_t pad;
-  uint32_t data[kUploadWords];
+  uint32_t data[W];
 };
 
-__global__ __launch_bounds__(256) void k_upload(uint32_t *dst, UploadChunk c) {
-  for (uint32_t i = threadIdx.x; i < c.words; i += 256) dst[i] = c.data[i];
+template <uint32_t W>
+__global__ __launch_bounds__(256) void k_upload(uint32_t *dst, UploadChunk<W> c) {
+  const uint32_t i0 = blockIdx.x * 1024;
+  const uint32_t i1 = min(c.words, i0 + 1024);
+  for (uint32_t i = i0 + threadIdx.x; i < i1; i += 256) dst[i] = c.data[i];
+}
+
+template <uint32_t W>
+hipError_t upload_chunk(uint32_t *dst, const uint8_t *src, uint32_t words, hipStream_t st) {
+  UploadChunk<W> c;
+  c.words = words;
+  c.pad = 0;
+  __builtin_memcpy(c.data, src, (size_t)words * 4);
+  hipLaunchKernelGGL(k_upload<W>, dim3((words + 1023) / 1024), dim3(256), 0, st, dst, c);
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -27,13 +44,13 @@ hipError_t launch_upload(uint8_t *dst, const uint8_t *src, size_t bytes, uint32_
                          size_t /*zero_words*/, hipStream_t st) {
   // `bytes` is a multiple of 4 (the plan is built from 4- and 8-byte fields).
   const size_t words = bytes / 4;
-  for (size_t w0 = 0; w0 < words; w0 += kUploadWords) {
-    UploadChunk c;
-    c.words = (uint32_t)((words - w0) < (size_t)kUploadWords ? (words - w0) : kUploadWords);
-    c.pad = 0;
-    __builtin_memcpy(c.data, src + w0 * 4, (size_t)c.words * 4);
-    hipLaunchKernelGGL(k_upload, dim3(1), dim3(256), 0, st, reinterpret_cast<uint32_t *>(dst) + w0, c);
-    hipError_t e = hipGetLastError();
+  for (size_t w0 = 0; w0 < words; w0 += kBigWords) {
+    const uint32_t n = (uint32_t)((words - w0) < (size_t)kBigWords ? (words - w0) : kBigWords);
+    uint32_t *d = reinterpret_cast<uint32_t *>(dst) + w0;
+    const uint8_t *s = src + w0 * 4;
+    const hipError_t e = n <= kSmallWords ? upload_chunk<kSmallWords>(d, s, n, st)
+                         : n <= kMidWords ? upload_chunk<kMidWords>(d, s, n, st)
+                                          : upload_chunk<kBigWords>(d, s, n, st);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

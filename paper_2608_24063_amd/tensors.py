@@ -60,16 +60,22 @@ class PruneCall:
 
     def run(self, events=None) -> None:
         """Enqueue viscache_prune; with `events` (VC_PRUNE_EVENTS torch.cuda.Event
-        objects created with enable_timing=True) the stages are bracketed."""
+        objects created with enable_timing=True, or raw hipEvent_t handles as
+        ints) the stages are bracketed."""
         drop = [_addr(t) for t in self.drop_out] if self.drop_out else None
         if events is None:
             viscache_prune(*self._args(), drop_out=drop)
         else:
             assert len(events) == VC_PRUNE_EVENTS
+            handles = []
             for e in events:
+                if isinstance(e, int):
+                    handles.append(e)
+                    continue
                 if e.cuda_event == 0:
                     e.record()  # materialise the handle
-            viscache_prune_staged(*self._args(), [e.cuda_event for e in events], drop_out=drop)
+                handles.append(e.cuda_event)
+            viscache_prune_staged(*self._args(), handles, drop_out=drop)
 
     def unit_rows(self, l: int, b: int, g: int):
         """Row range of (layer, sequence, kv head) in layer l's outputs."""
