@@ -213,24 +213,19 @@ __device__ __forceinline__ void fuse_tile(FuseState<D> &st, const uint16_t *vt, 
 // Workgroup = (fusion unit, 128 kept rows); wave w owns kept rows
 // w*32 + nb*16 + [0, 16) for nb = 0, 1, so every operand read from LDS feeds
 // two matrix instructions.
-template <int D, bool VFP32>
-__global__ __launch_bounds__(256, 2) void k_fuse(PrunePlan p) {
-  constexpr int KS = D / 32, MB = D / 16, NB = 2;
-  __shared__ __attribute__((aligned(16))) uint16_t vr[2][kDropTile * kPitchRow<D>];
+template <int D>
+using DropTiles = uint16_t[2][kDropTile * kPitchRow<D>];
 
-  // Block -> (unit, tile): block b runs on XCD b % 8; each XCD takes every
-  // 8th unit of the longest-first list, all tiles of a unit on the same XCD
-  // (they share the unit's dropped rows in L2).
-  const uint32_t x = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
-  const int rank = (int)(x + kXcds * (slot / p.nfuse));
-  const int tile = (int)(slot % p.nfuse);
-  if (rank >= p.nfunits) return;
+// One fusion job: kept rows [128 tile, 128 tile + 128) of the unit of rank
+// `rank` in the fusion unit list.
+template <int D, bool VFP32>
+__device__ __forceinline__ void fuse_job(const PrunePlan &p, int rank, int tile, DropTiles<D> &vr) {
+  constexpr int KS = D / 32, MB = D / 16, NB = 2;
   const u32x4 *rec = reinterpret_cast<const u32x4 *>(p.funit + rank);
   const u32x4 r0 = ld16(rec), r1 = ld16(rec + 1), r2 = ld16(rec + 2), r3 = ld16(rec + 3);
   auto ptr = [](uint32_t lo, uint32_t hi) { return (uint64_t)lo | ((uint64_t)hi << 32); };
   const int k = (int)r3.x, r = (int)r3.y, n = (int)r3.z;
-  const int j0 = tile * kFuseRows;
-  if (j0 >= k) return;
+  const int j0 = tile * kFuseRows;  // < k: the host lists only non-empty jobs
   const uint16_t *Kin = reinterpret_cast<const uint16_t *>(ptr(r0.x, r0.y));
   const uint16_t *Vin = reinterpret_cast<const uint16_t *>(ptr(r0.z, r0.w));
   uint16_t *Kout = reinterpret_cast<uint16_t *>(ptr(r1.x, r1.y)) + (int64_t)j0 * D;
@@ -400,6 +395,21 @@ __global__ __launch_bounds__(256, 2) void k_fuse(PrunePlan p) {
   }
 }
 
+// Persistent workgroups: block b walks the job list the host packed for it
+// (block b runs on XCD b % 8, which holds the L2 lines of its units).  Wave w
+// owns kept rows w*32 + nb*16 + [0, 16) of a job for nb = 0, 1, so every
+// operand read from LDS feeds two matrix instructions.
+template <int D, bool VFP32>
+__global__ __launch_bounds__(256, 2) void k_fuse(PrunePlan p) {
+  __shared__ __attribute__((aligned(16))) DropTiles<D> vr;
+  const int j0 = ldg(p.fwoff + blockIdx.x), j1 = ldg(p.fwoff + blockIdx.x + 1);
+  for (int j = j0; j < j1; ++j) {
+    const int code = ldg(p.fwjob + j);
+    fuse_job<D, VFP32>(p, code >> 8, code & 255, vr);
+    __syncthreads();  // the next job restages the LDS tiles
+  }
+}
+
 template <int D>
 hipError_t launch_fuse_d(const PrunePlan &p, hipStream_t st, uint32_t grid) {
   if (p.v_fp32)
@@ -412,8 +422,8 @@ hipError_t launch_fuse_d(const PrunePlan &p, hipStream_t st, uint32_t grid) {
 }  // namespace
 
 hipError_t launch_fuse(const PrunePlan &p, hipStream_t st) {
-  if (p.nfunits == 0) return hipSuccess;
-  const uint32_t grid = (uint32_t)kXcds * (uint32_t)((p.nfunits + kXcds - 1) / kXcds) * (uint32_t)p.nfuse;
+  if (p.nfunits == 0 || p.nfwg <= 0) return hipSuccess;
+  const uint32_t grid = (uint32_t)p.nfwg;
   return p.d == 128 ? launch_fuse_d<128>(p, st, grid) : launch_fuse_d<64>(p, st, grid);
 }
 

@@ -118,20 +118,17 @@ __device__ __forceinline__ void stats_tile(const uint16_t *kl, const bf16x8 (&bq
       a[kb][s] = as_bf16x8(*reinterpret_cast<const u32x4 *>(kl + (kb * 16 + lr) * P + 32 * s + 8 * lg));
   f32x4 cur[4], nxt[4];
 #pragma unroll
-  for (int kb = 0; kb < 4; ++kb) {
-    cur[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < KS; ++s)
 #pragma unroll
-    for (int s = 0; s < KS; ++s) cur[kb] = mfma_bf16(a[kb][s], bq[0][s], cur[kb]);
-  }
+    for (int kb = 0; kb < 4; ++kb) cur[kb] = mfma_bf16(a[kb][s], bq[0][s], s == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : cur[kb]);
 #pragma unroll
   for (int qb = 0; qb < 4; ++qb) {
     if (qb + 1 < 4) {
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        nxt[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int s = 0; s < KS; ++s)
 #pragma unroll
-        for (int s = 0; s < KS; ++s) nxt[kb] = mfma_bf16(a[kb][s], bq[qb + 1][s], nxt[kb]);
-      }
+        for (int kb = 0; kb < 4; ++kb)
+          nxt[kb] = mfma_bf16(a[kb][s], bq[qb + 1][s], s == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : nxt[kb]);
     }
     stats_rows<MASK>(cur, m[qb], sum[qb], tb, k1, lg, sc);
     if (qb + 1 < 4) interleave_mfma_valu<4 * KS, 4>();
@@ -158,7 +155,9 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p) {
   const int lr = lane & 15, lg = lane >> 4;
   const float sc = p.sc;
 
-  const int span = ((n + p.nks - 1) / p.nks + 15) & ~15;
+  // Key splits are whole tiles, so only the last split of a unit can end in
+  // a partial tile.
+  const int span = ((n + p.nks - 1) / p.nks + kKeyTile - 1) & ~(kKeyTile - 1);
   const int k0 = min(n, ks * span), k1 = min(n, k0 + span);
 
   const uint16_t *K = reinterpret_cast<const uint16_t *>(ldg(p.lp + LP_K_IN * p.L + ls)) +
@@ -169,6 +168,7 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p) {
 
   // Query rows -> bf16 B operands (round to nearest even), zero past R.
   const int row0 = qg * kStatsRows + w * 64;
+  const bool active = row0 < p.R;  // wave-uniform: waves of padding rows only stage tiles
   bf16x8 bq[4][KS];
 #pragma unroll
   for (int qb = 0; qb < 4; ++qb) {
@@ -203,13 +203,17 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p) {
   for (int t = 0; t < ntiles; ++t) {
     const int tb = k0 + t * kKeyTile;
     if (t + 1 < ntiles) tr.load(K, tb + kKeyTile, k1, tid);
-    if (tb + kKeyTile <= k1)
-      stats_tile<D, false>(kt[t & 1], bq, m, sum, tb, k1, lr, lg, sc);
-    else
-      stats_tile<D, true>(kt[t & 1], bq, m, sum, tb, k1, lr, lg, sc);
+    if (active) {
+      if (tb + kKeyTile <= k1)
+        stats_tile<D, false>(kt[t & 1], bq, m, sum, tb, k1, lr, lg, sc);
+      else
+        stats_tile<D, true>(kt[t & 1], bq, m, sum, tb, k1, lr, lg, sc);
+    }
     if (t + 1 < ntiles) tr.store(kt[(t + 1) & 1], tid);
     __syncthreads();
   }
+
+  if (!active) return;
 
   // Combine the four lane groups that share a query row, then store.
 #pragma unroll
@@ -230,14 +234,14 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p) {
 }
 
 // ---------------------------------------------------------------------------
-// Pass 2: column sums.  Workgroup = (unit, 256-key chunk).  Wave w owns keys
-// chunk*256 + w*64 + [0, 64) as B operands; the G*W query rows (bf16 copies
+// Pass 2: column sums.  Workgroup = (unit, 128-key chunk).  Wave w owns keys
+// chunk*128 + w*32 + [0, 32) as B operands; the G*W query rows (bf16 copies
 // written by pass 1) stream through LDS 64 rows at a time as A operands, so the
 // product is Z (queries x keys): lane l sees key l%16 of each 16-key block and
 // rows 4*(l/16)+i, and accumulates exp2(z*sc - m_r) / sum_r per key.
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ __launch_bounds__(256, 2) void k_score_colsum(PrunePlan p) {
+__global__ __launch_bounds__(256, 3) void k_score_colsum(PrunePlan p) {
   constexpr int KS = D / 32;
   constexpr int P = kPitch<D>;
   constexpr int kMaxR = 1024;
@@ -264,10 +268,11 @@ __global__ __launch_bounds__(256, 2) void k_score_colsum(PrunePlan p) {
                        ((int64_t)b * p.Hq + (int64_t)g * p.G) * p.W * D;
 
   // Keys of this wave as B operands.
-  const int key0 = c * kColKeys + w * 64;
-  bf16x8 bk[4][KS];
+  const int key0 = c * kColKeys + w * 32;
+  const bool active = key0 < n;  // wave-uniform
+  bf16x8 bk[2][KS];
 #pragma unroll
-  for (int kb = 0; kb < 4; ++kb) {
+  for (int kb = 0; kb < 2; ++kb) {
     const int key = key0 + kb * 16 + lr;
 #pragma unroll
     for (int s = 0; s < KS; ++s)
@@ -278,18 +283,24 @@ __global__ __launch_bounds__(256, 2) void k_score_colsum(PrunePlan p) {
 
   // Row statistics: merge the key splits of pass 1.  Rows past R get a
   // reference of +inf so they contribute exp2(-inf) = 0.
+  // All partials of a row are loaded in one batch (nks <= kMaxSplits).
   for (int r = tid; r < Rpad; r += 256) {
     float2 st = make_float2(__builtin_inff(), 0.f);
     if (r < R) {
       const float2 *pr = p.part + (int64_t)u * p.nks * R + r;
+      float2 q[kMaxSplits];
+#pragma unroll
+      for (int k = 0; k < kMaxSplits; ++k)
+        q[k] = k < p.nks ? ldg(pr + (int64_t)k * R) : make_float2(kNegInf, 0.f);
       float M = kNegInf;
-      for (int k = 0; k < p.nks; ++k) M = fmaxf(M, ldg(pr + (int64_t)k * R).x);
+#pragma unroll
+      for (int k = 0; k < kMaxSplits; ++k) M = fmaxf(M, q[k].x);
       float s = 0.f;
-      if (M != kNegInf)
-        for (int k = 0; k < p.nks; ++k) {
-          const float2 q = ldg(pr + (int64_t)k * R);
-          if (q.x != kNegInf) s += q.y * fast_exp2(q.x - M);
-        }
+      if (M != kNegInf) {
+#pragma unroll
+        for (int k = 0; k < kMaxSplits; ++k)
+          if (q[k].x != kNegInf) s += q[k].y * fast_exp2(q[k].x - M);
+      }
       st = make_float2(M == kNegInf ? __builtin_inff() : M, s > 0.f ? 1.f / s : 0.f);
     }
     rs[r] = st;
@@ -297,53 +308,47 @@ __global__ __launch_bounds__(256, 2) void k_score_colsum(PrunePlan p) {
   tr.store(qt[0], tid);
   __syncthreads();
 
-  float col[4] = {0.f, 0.f, 0.f, 0.f};
+  float col[2] = {0.f, 0.f};
   const int ntiles = Rpad / 64;
   for (int t = 0; t < ntiles; ++t) {
     if (t + 1 < ntiles) tr.load(Qb, (t + 1) * 64, R, tid);
-    const uint16_t *ql = qt[t & 1];
-    // Matrix work of query block qb+1 is issued ahead of the exp work of qb.
-    f32x4 cur[4], nxt[4];
+    if (active) {
+      const uint16_t *ql = qt[t & 1];
+      // Four query blocks x two key blocks: eight accumulation chains.
+      f32x4 acc[4][2];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) cur[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int s = 0; s < KS; ++s) {
+        bf16x8 a[4];
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      const bf16x8 a = as_bf16x8(*reinterpret_cast<const u32x4 *>(ql + lr * P + 32 * s + 8 * lg));
+        for (int qb = 0; qb < 4; ++qb)
+          a[qb] = as_bf16x8(*reinterpret_cast<const u32x4 *>(ql + (qb * 16 + lr) * P + 32 * s + 8 * lg));
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) cur[kb] = mfma_bf16(a, bk[kb][s], cur[kb]);
-    }
+        for (int qb = 0; qb < 4; ++qb)
 #pragma unroll
-    for (int qb = 0; qb < 4; ++qb) {
-      if (qb + 1 < 4) {
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) nxt[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int s = 0; s < KS; ++s) {
-          const bf16x8 a = as_bf16x8(*reinterpret_cast<const u32x4 *>(ql + ((qb + 1) * 16 + lr) * P + 32 * s + 8 * lg));
-#pragma unroll
-          for (int kb = 0; kb < 4; ++kb) nxt[kb] = mfma_bf16(a, bk[kb][s], nxt[kb]);
-        }
+          for (int kb = 0; kb < 2; ++kb)
+            acc[qb][kb] = mfma_bf16(a[qb], bk[kb][s], s == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : acc[qb][kb]);
       }
-      const int rbase = t * 64 + qb * 16 + 4 * lg;
-      const f32x4 s01 = *reinterpret_cast<const f32x4 *>(&rs[rbase]);
-      const f32x4 s23 = *reinterpret_cast<const f32x4 *>(&rs[rbase + 2]);
-      const float mr[4] = {s01.x, s01.z, s23.x, s23.z}, ir[4] = {s01.y, s01.w, s23.y, s23.w};
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
+      for (int qb = 0; qb < 4; ++qb) {
+        const int rbase = t * 64 + qb * 16 + 4 * lg;
+        const f32x4 s01 = *reinterpret_cast<const f32x4 *>(&rs[rbase]);
+        const f32x4 s23 = *reinterpret_cast<const f32x4 *>(&rs[rbase + 2]);
+        const float mr[4] = {s01.x, s01.z, s23.x, s23.z}, ir[4] = {s01.y, s01.w, s23.y, s23.w};
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          col[kb] = fmaf(fast_exp2(fmaf(cur[kb][i], sc, -mr[i])), ir[i], col[kb]);
-      if (qb + 1 < 4) interleave_mfma_valu<4 * KS, 3>();
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) cur[kb] = nxt[kb];
+          for (int i = 0; i < 4; ++i)
+            col[kb] = fmaf(fast_exp2(fmaf(acc[qb][kb][i], sc, -mr[i])), ir[i], col[kb]);
+      }
     }
     if (t + 1 < ntiles) tr.store(qt[(t + 1) & 1], tid);
     __syncthreads();
   }
+  if (!active) return;
 
   float *S = p.S + (int64_t)ls * p.Ntot * p.Hkv + toff * p.Hkv + (int64_t)g * n;
 #pragma unroll
-  for (int kb = 0; kb < 4; ++kb) {
+  for (int kb = 0; kb < 2; ++kb) {
     float v = col[kb];
     v += shfl_xor(v, 16);
     v += shfl_xor(v, 32);

@@ -26,11 +26,12 @@ struct Layout {
   int64_t Ntot;
   std::vector<int32_t> n, k, ns;       // n[B], k[B*L], ns[B*L]
   std::vector<int32_t> funit;          // fusion units, longest drop list first
+  std::vector<int32_t> fwoff, fwjob;   // fusion workgroup job lists (CSR): job = rank << 8 | tile
   std::vector<int64_t> toff, orow, drow;
   // workspace regions (byte offsets)
   size_t off_plan, plan_bytes, off_qbf, off_part, off_S, off_gs, off_drop, total;
   // offsets inside the plan blob
-  size_t p_lp, p_nb, p_toff, p_kk, p_ns, p_orow, p_drow, p_funit;
+  size_t p_lp, p_nb, p_toff, p_kk, p_ns, p_orow, p_drow, p_funit, p_fwoff, p_fwjob;
 };
 
 vc_status check_shape(const vc_shape *s) {
@@ -97,10 +98,10 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   y.nqg = (y.R + kStatsRows - 1) / kStatsRows;
   const int64_t base = std::max<int64_t>(1, units * y.nqg);
   // Key splits so that the statistics pass runs in one round of resident
-  // workgroups (256 CUs x 2): a second, partial round costs a full workgroup
-  // time for a fraction of the work.
-  int64_t nks = std::max<int64_t>(1, 512 / base);
-  nks = std::min<int64_t>(nks, 8);
+  // workgroups: a second, partial round costs a full workgroup time for a
+  // fraction of the work.
+  int64_t nks = std::max<int64_t>(1, kScoreSlots / base);
+  nks = std::min<int64_t>(nks, kMaxSplits);
   nks = std::min<int64_t>(nks, std::max(1, (y.nmax + kKeyTile - 1) / kKeyTile));
   y.nks = (int32_t)std::max<int64_t>(1, nks);
   y.ncol = std::max(1, (y.nmax + kColKeys - 1) / kColKeys);
@@ -119,6 +120,51 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   };
   std::stable_sort(y.funit.begin(), y.funit.end(),
                    [&](int32_t a, int32_t c) { return drops(a) > drops(c); });
+  // Fusion jobs (unit, 128 kept rows) packed into persistent workgroups.  Unit
+  // of rank r goes to XCD r % 8 (all its jobs share its dropped rows in L2);
+  // inside an XCD, jobs are placed longest first on the least loaded of its
+  // workgroups (block b runs on XCD b % 8).  Cost of a job: its dropped
+  // tiles plus the fixed start-up of a job, in tile units.
+  {
+    constexpr int32_t kFuseSlots = 512;  // resident fusion workgroups (256 CUs x 2)
+    constexpr double kJobStart = 4.0;
+    struct Job { double cost; int32_t code; };
+    std::vector<std::vector<Job>> xj(kXcdsHost);
+    int64_t njobs = 0;
+    for (size_t rk = 0; rk < y.funit.size(); ++rk) {
+      const int32_t u = y.funit[rk];
+      const int32_t l = u / (y.Hkv * y.B), b = (u / y.Hkv) % y.B;
+      const int32_t kk = y.k[(size_t)b * y.L + l];
+      const int32_t rr = y.ns[(size_t)b * y.L + l] - kk;
+      const double cost = kJobStart + (double)((rr + kDropTile - 1) / kDropTile);
+      for (int32_t t = 0; t * kFuseRows < kk; ++t) {
+        xj[rk % kXcdsHost].push_back({cost, (int32_t)(rk << 8) | t});
+        ++njobs;
+      }
+    }
+    const int32_t per_xcd = (int32_t)std::max<int64_t>(
+        1, std::min<int64_t>(kFuseSlots / kXcdsHost, (njobs + kXcdsHost - 1) / kXcdsHost));
+    const int32_t nwg = per_xcd * kXcdsHost;
+    std::vector<std::vector<int32_t>> lists(nwg);
+    for (int32_t x = 0; x < kXcdsHost; ++x) {
+      auto &jl = xj[x];
+      std::stable_sort(jl.begin(), jl.end(), [](const Job &a, const Job &c) { return a.cost > c.cost; });
+      std::vector<double> load(per_xcd, 0.0);
+      for (const Job &j : jl) {
+        int32_t best = 0;
+        for (int32_t i = 1; i < per_xcd; ++i)
+          if (load[i] < load[best]) best = i;
+        load[best] += j.cost;
+        lists[x + kXcdsHost * best].push_back(j.code);
+      }
+    }
+    y.fwoff.assign(1, 0);
+    y.fwjob.clear();
+    for (int32_t w = 0; w < nwg; ++w) {
+      y.fwjob.insert(y.fwjob.end(), lists[w].begin(), lists[w].end());
+      y.fwoff.push_back((int32_t)y.fwjob.size());
+    }
+  }
 
   // Plan blob.
   size_t o = 0;
@@ -131,6 +177,8 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   y.p_ns = o; o += sizeof(int32_t) * y.B * y.L;
   o = (o + 15) & ~size_t(15);
   y.p_funit = o; o += sizeof(FuseUnit) * y.funit.size();
+  y.p_fwoff = o; o += sizeof(int32_t) * y.fwoff.size();
+  y.p_fwjob = o; o += sizeof(int32_t) * y.fwjob.size();
   o = (o + 7) & ~size_t(7);
   y.plan_bytes = o;
 
@@ -251,6 +299,8 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   std::memcpy(blob.data() + y.p_nb, y.n.data(), sizeof(int32_t) * y.n.size());
   std::memcpy(blob.data() + y.p_kk, y.k.data(), sizeof(int32_t) * y.k.size());
   std::memcpy(blob.data() + y.p_ns, y.ns.data(), sizeof(int32_t) * y.ns.size());
+  std::memcpy(blob.data() + y.p_fwoff, y.fwoff.data(), sizeof(int32_t) * y.fwoff.size());
+  if (!y.fwjob.empty()) std::memcpy(blob.data() + y.p_fwjob, y.fwjob.data(), sizeof(int32_t) * y.fwjob.size());
   {
     // Fusion unit records: absolute row addresses, so the fusion kernel
     // needs one dependent load before its index loads.
@@ -283,6 +333,7 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   pl.R = y.R; pl.h = y.h; pl.Ls = y.Ls; pl.mode = y.mode; pl.v_fp32 = y.vfp32;
   pl.nqg = y.nqg; pl.nks = y.nks; pl.ncol = y.ncol; pl.nfuse = y.nfuse; pl.nmax = y.nmax;
   pl.nfunits = (int32_t)y.funit.size();
+  pl.nfwg = (int32_t)y.fwoff.size() - 1;
   pl.sc = (float)(1.4426950408889634 / std::sqrt((double)y.d));
   pl.tc = (float)(1.4426950408889634 / (double)params->tau);
   pl.mu = params->mu;
@@ -296,6 +347,8 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   pl.orow = reinterpret_cast<const int64_t *>(pb + y.p_orow);
   pl.drow = reinterpret_cast<const int64_t *>(pb + y.p_drow);
   pl.funit = reinterpret_cast<const FuseUnit *>(pb + y.p_funit);
+  pl.fwoff = reinterpret_cast<const int32_t *>(pb + y.p_fwoff);
+  pl.fwjob = reinterpret_cast<const int32_t *>(pb + y.p_fwjob);
   pl.qbf = reinterpret_cast<uint16_t *>(ws + y.off_qbf);
   pl.part = reinterpret_cast<float2 *>(ws + y.off_part);
   pl.rowst = nullptr;

@@ -13,12 +13,15 @@ enum { LP_K_IN = 0, LP_V_IN, LP_Q, LP_K_OUT, LP_V_OUT, LP_IDX, LP_DROP, LP_COUNT
 // Tile sizes shared by host-side grid sizing and the kernels.
 constexpr int kStatsRows = 256;   // query rows per stats workgroup (4 waves x 64)
 constexpr int kKeyTile = 64;      // keys staged per LDS tile
-constexpr int kColKeys = 256;     // keys per column-sum workgroup (4 waves x 64)
+constexpr int kColKeys = 128;     // keys per column-sum workgroup (4 waves x 32)
+constexpr int kScoreSlots = 512;  // resident stats workgroups (256 CUs x 2)
+constexpr int kMaxSplits = 8;     // key splits of the stats pass
 constexpr int kFuseRows = 128;    // kept rows per fusion workgroup (4 waves x 32)
 constexpr int kDropTile = 64;     // dropped rows staged per LDS tile
 constexpr int kSelectThreads = 512;
 constexpr int kSelectPerThread = 64;  // => n <= 32768 tokens per sequence
 constexpr int kMaxTokens = kSelectThreads * kSelectPerThread;
+constexpr int kXcdsHost = 8;      // MI355X accelerator dies (host-side grid planning)
 
 // One fusion unit (layer, sequence, kv head) with kept rows, as the fusion
 // kernel reads it: absolute addresses of the unit's first rows and its sizes.
@@ -41,7 +44,8 @@ struct PrunePlan {
   int32_t nqg, nks;   // stats grid: query groups x key splits per unit
   int32_t ncol;       // column-sum chunks per unit (max over sequences)
   int32_t nfuse;      // fusion tiles per unit (max over units)
-  int32_t nfunits;    // units with kept rows (fusion grid = 8 x ceil(nfunits/8) x nfuse)
+  int32_t nfunits;    // units with kept rows
+  int32_t nfwg;       // fusion workgroups (persistent; each walks its job list)
   int32_t nmax;       // max n_b
   float sc;           // log2(e) / sqrt(d)
   float tc;           // log2(e) / tau
@@ -55,6 +59,8 @@ struct PrunePlan {
   const int64_t *orow;  // [L*(B+1)] output row offsets per layer
   const int64_t *drow;  // [L*(B+1)] dropped-row offsets per layer
   const FuseUnit *funit; // [nfunits] fusion units, most dropped rows first
+  const int32_t *fwoff;  // [nfwg+1] job list offsets per fusion workgroup
+  const int32_t *fwjob;  // fusion jobs: unit rank << 8 | 128-row tile
   uint16_t *qbf;        // [Ls][B][Hq][W][d] window queries in bf16
   float2 *part;         // [U][nks][R] partial row statistics (max*sc, sum)
   float2 *rowst;        // [U][R] row statistics (max*sc, 1/sum)
