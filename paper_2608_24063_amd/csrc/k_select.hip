@@ -3,13 +3,12 @@
 // descending then token index ascending; the first k tokens are kept, the next
 // n_surv - k are dropped (their values get fused), the rest are discarded.
 //
-// One workgroup per unit; each thread holds a contiguous run of PER scores in
-// registers.  Scores are non-negative fp32, so their bit patterns order like
-// the values.  The k-th largest bit pattern is found exactly by a 31-step
-// bisection over the bit positions (both cuts in the same loop; counts come
-// from wave ballots and scalar popcounts), ties at the threshold go to the
-// lowest indices, and a block-wide prefix sum compacts kept and dropped
-// indices in ascending token order.
+// One workgroup per unit (256 to 1024 threads, by the longest sequence); each
+// thread holds a contiguous run of up to PER scores in registers.  Scores are non-negative fp32, so their bit
+// patterns order like the values.  The k-th and n_surv-th largest bit patterns
+// are found exactly by a 31-round bisection (both cuts together), ties at a
+// threshold go to the lowest indices, and block-wide prefix sums (DPP wave
+// scans) compact kept and dropped indices in ascending token order.
 #include "vc_device.h"
 #include "vc_internal.h"
 
@@ -17,41 +16,43 @@ namespace vc {
 
 namespace {
 
+
+// Inclusive prefix sum over the 64 lanes of a wave (DPP: shifts within rows
+// of 16 lanes, then row broadcasts).
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, false);  // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, false);  // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, false);  // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, false);  // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return x;
+}
+
 // Exclusive prefix over the block of four counters per thread, plus totals.
-template <int THREADS>
+template <int kWaves>
 __device__ __forceinline__ void block_scan4(const uint32_t v[4], uint32_t excl[4], uint32_t tot[4],
-                                            uint4 *sh) {
-  const int tid = threadIdx.x, lane = tid & 63;
-  sh[tid] = make_uint4(v[0], v[1], v[2], v[3]);
-  __syncthreads();
-  if (tid < 64) {
-    constexpr int per = THREADS / 64;
-    uint4 run = make_uint4(0, 0, 0, 0);
+                                            uint32_t (*wt)[kWaves]) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  uint32_t inc[4];
 #pragma unroll
-    for (int i = 0; i < per; ++i) {
-      const uint4 x = sh[lane * per + i];
-      run.x += x.x; run.y += x.y; run.z += x.z; run.w += x.w;
-    }
-    uint4 inc = run;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const uint32_t a = __shfl_up(inc.x, off, 64), b = __shfl_up(inc.y, off, 64);
-      const uint32_t c = __shfl_up(inc.z, off, 64), d = __shfl_up(inc.w, off, 64);
-      if (lane >= off) { inc.x += a; inc.y += b; inc.z += c; inc.w += d; }
-    }
-    uint4 base = make_uint4(inc.x - run.x, inc.y - run.y, inc.z - run.z, inc.w - run.w);
-#pragma unroll
-    for (int i = 0; i < per; ++i) {
-      const uint4 x = sh[lane * per + i];
-      sh[lane * per + i] = base;
-      base.x += x.x; base.y += x.y; base.z += x.z; base.w += x.w;
-    }
-    if (lane == 63) sh[THREADS] = inc;
+  for (int c = 0; c < 4; ++c) {
+    inc[c] = wave_incl_scan(v[c]);
+    if (lane == 63) wt[c][w] = inc[c];
   }
   __syncthreads();
-  const uint4 e = sh[tid], t = sh[THREADS];
-  excl[0] = e.x; excl[1] = e.y; excl[2] = e.z; excl[3] = e.w;
-  tot[0] = t.x; tot[1] = t.y; tot[2] = t.z; tot[3] = t.w;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    uint32_t before = 0, all = 0;
+#pragma unroll
+    for (int q = 0; q < kWaves; ++q) {
+      const uint32_t x = wt[c][q];
+      before += q < w ? x : 0u;
+      all += x;
+    }
+    excl[c] = before + inc[c] - v[c];
+    tot[c] = all;
+  }
   __syncthreads();
 }
 
@@ -59,11 +60,15 @@ __device__ __forceinline__ uint32_t count_wave(bool pred) {
   return (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(pred));
 }
 
-template <int THREADS, int PER>
-__global__ __launch_bounds__(THREADS) void k_select(PrunePlan p) {
-  constexpr int kWaves = THREADS / 64;
-  __shared__ uint32_t red[2][kWaves][2];
-  __shared__ uint4 scan_sh[THREADS + 1];
+// One unit: the k-th and n_surv-th largest score bit patterns are found
+// exactly by bisection over the 31 bit positions, both cuts in the same
+// rounds; each wave counts its keys with ballots, and the wave counts meet in
+// LDS once per round.
+template <int kThreads, int PER>
+__global__ __launch_bounds__(kThreads) void k_select(PrunePlan p) {
+  constexpr int kWaves = kThreads / 64;
+  __shared__ __attribute__((aligned(16))) uint32_t red[2][2][kWaves];  // [round parity][cut][wave]
+  __shared__ uint32_t wt[4][kWaves];
 
   const int u = blockIdx.x;  // ((l * B) + b) * Hkv + g, l < h
   const int g = u % p.Hkv;
@@ -79,7 +84,7 @@ __global__ __launch_bounds__(THREADS) void k_select(PrunePlan p) {
   const float *S = p.mode ? p.gs + toff
                           : p.S + (int64_t)l * p.Ntot * p.Hkv + toff * p.Hkv + (int64_t)g * n;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int per = (n + THREADS - 1) / THREADS;  // <= PER
+  const int per = (n + kThreads - 1) / kThreads;  // <= PER
   const int v0 = tid * per;
   const int cnt = max(0, min(per, n - v0));
 
@@ -94,30 +99,34 @@ __global__ __launch_bounds__(THREADS) void k_select(PrunePlan p) {
     key[i] = (x & 0x80000000u) ? 0x7FFFFFFFu : x;
   }
 
-  // Bisection for the k-th and n_surv-th largest keys.
-  uint32_t tk = 0, ts = 0;
+  uint32_t pre[2] = {0u, 0u};
+  const uint32_t need[2] = {(uint32_t)k, (uint32_t)nsv};
+#pragma unroll 1
   for (int bit = 30, it = 0; bit >= 0; --bit, ++it) {
-    const uint32_t ck = tk | (1u << bit), cs = ts | (1u << bit);
-    uint32_t nk = 0, nsu = 0;
+    const uint32_t ck = pre[0] | (1u << bit), cs = pre[1] | (1u << bit);
+    uint32_t nk = 0, ns = 0;
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       nk += count_wave(key[i] >= ck);
-      nsu += count_wave(key[i] >= cs);
+      ns += count_wave(key[i] >= cs);
     }
     if (lane == 0) {
-      red[it & 1][w][0] = nk;
-      red[it & 1][w][1] = nsu;
+      red[it & 1][0][w] = nk;
+      red[it & 1][1][w] = ns;
     }
     __syncthreads();
-    uint32_t tnk = 0, tns = 0;
+    uint32_t tk = 0, ts = 0;
 #pragma unroll
-    for (int i = 0; i < kWaves; ++i) {
-      tnk += red[it & 1][i][0];
-      tns += red[it & 1][i][1];
+    for (int q = 0; q < kWaves; q += 4) {  // kWaves is a multiple of 4
+      const uint4 a = *reinterpret_cast<const uint4 *>(&red[it & 1][0][q]);
+      const uint4 c = *reinterpret_cast<const uint4 *>(&red[it & 1][1][q]);
+      tk += a.x + a.y + a.z + a.w;
+      ts += c.x + c.y + c.z + c.w;
     }
-    if (tnk >= (uint32_t)k) tk = ck;
-    if (tns >= (uint32_t)nsv) ts = cs;
+    if (tk >= need[0]) pre[0] = ck;
+    if (ts >= need[1]) pre[1] = cs;
   }
+  const uint32_t tk = k > 0 ? pre[0] : 0xFFFFFFFFu, ts = pre[1];
 
   // Counts above and at each threshold; ties fill in ascending index order.
   uint32_t c4[4] = {0, 0, 0, 0};
@@ -129,15 +138,13 @@ __global__ __launch_bounds__(THREADS) void k_select(PrunePlan p) {
       c4[2] += key[i] > ts;
       c4[3] += key[i] == ts;
     }
-  uint32_t ex[4], tot[4];
-  block_scan4<THREADS>(c4, ex, tot, scan_sh);
-  const uint32_t need_k = k > 0 ? (uint32_t)k - tot[0] : 0u;
-  const uint32_t need_s = (uint32_t)nsv - tot[2];
+  uint32_t ex[4], tot4[4];
+  block_scan4<kWaves>(c4, ex, tot4, wt);
+  const uint32_t need_k = k > 0 ? (uint32_t)k - tot4[0] : 0u;
+  const uint32_t need_s = (uint32_t)nsv - tot4[2];
   uint32_t ek = ex[1], es = ex[3];
 
-  uint32_t keepmask[(PER + 31) / 32], dropmask[(PER + 31) / 32];
-#pragma unroll
-  for (int j = 0; j < (PER + 31) / 32; ++j) keepmask[j] = dropmask[j] = 0u;
+  uint32_t keepmask = 0u, dropmask = 0u;
   uint32_t nkeep = 0, ndrop = 0;
 #pragma unroll
   for (int i = 0; i < PER; ++i)
@@ -150,12 +157,12 @@ __global__ __launch_bounds__(THREADS) void k_select(PrunePlan p) {
       }
       const bool sv = x > ts || (x == ts && es < need_s);
       if (x == ts) ++es;
-      if (kp) { keepmask[i / 32] |= 1u << (i % 32); ++nkeep; }
-      else if (sv) { dropmask[i / 32] |= 1u << (i % 32); ++ndrop; }
+      if (kp) { keepmask |= 1u << i; ++nkeep; }
+      else if (sv) { dropmask |= 1u << i; ++ndrop; }
     }
 
   const uint32_t c2[4] = {nkeep, ndrop, 0, 0};
-  block_scan4<THREADS>(c2, ex, tot, scan_sh);
+  block_scan4<kWaves>(c2, ex, tot4, wt);
 
   int32_t *idx = reinterpret_cast<int32_t *>(ldg(p.lp + LP_IDX * p.L + l)) +
                  ldg(p.orow + l * (p.B + 1) + b) + (int64_t)g * k;
@@ -164,11 +171,11 @@ __global__ __launch_bounds__(THREADS) void k_select(PrunePlan p) {
   uint32_t pk = ex[0], pd = ex[1];
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
-    if ((keepmask[i / 32] >> (i % 32)) & 1u) {
+    if ((keepmask >> i) & 1u) {
       if (pk < (uint32_t)k) stg(idx + pk, (int32_t)(v0 + i));
       ++pk;
     }
-    if ((dropmask[i / 32] >> (i % 32)) & 1u) {
+    if ((dropmask >> i) & 1u) {
       if (pd < (uint32_t)r) stg(drop + pd, (int32_t)(v0 + i));
       ++pd;
     }
@@ -180,13 +187,13 @@ __global__ __launch_bounds__(THREADS) void k_select(PrunePlan p) {
 hipError_t launch_select(const PrunePlan &p, hipStream_t st) {
   const uint32_t grid = (uint32_t)p.h * p.B * p.Hkv;
   if (grid == 0) return hipSuccess;
-  // Smallest block that holds the longest sequence in registers.
+  // Smallest register run that holds the longest sequence.
   if (p.nmax <= 256 * 16)
     hipLaunchKernelGGL((k_select<256, 16>), dim3(grid), dim3(256), 0, st, p);
-  else if (p.nmax <= 256 * 32)
-    hipLaunchKernelGGL((k_select<256, 32>), dim3(grid), dim3(256), 0, st, p);
-  else if (p.nmax <= 512 * 32)
-    hipLaunchKernelGGL((k_select<512, 32>), dim3(grid), dim3(512), 0, st, p);
+  else if (p.nmax <= 512 * 16)
+    hipLaunchKernelGGL((k_select<512, 16>), dim3(grid), dim3(512), 0, st, p);
+  else if (p.nmax <= 1024 * 16)
+    hipLaunchKernelGGL((k_select<1024, 16>), dim3(grid), dim3(1024), 0, st, p);
   else
     hipLaunchKernelGGL((k_select<1024, 32>), dim3(grid), dim3(1024), 0, st, p);
   return hipGetLastError();

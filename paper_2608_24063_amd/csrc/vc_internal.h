@@ -18,8 +18,8 @@ constexpr int kScoreSlots = 512;  // resident stats workgroups (256 CUs x 2)
 constexpr int kMaxSplits = 8;     // key splits of the stats pass
 constexpr int kFuseRows = 128;    // kept rows per fusion workgroup (4 waves x 32)
 constexpr int kDropTile = 64;     // dropped rows staged per LDS tile
-constexpr int kSelectThreads = 512;
-constexpr int kSelectPerThread = 64;  // => n <= 32768 tokens per sequence
+constexpr int kSelectThreads = 1024;
+constexpr int kSelectPerThread = 32;  // => n <= 32768 tokens per sequence
 constexpr int kMaxTokens = kSelectThreads * kSelectPerThread;
 constexpr int kXcdsHost = 8;      // MI355X accelerator dies (host-side grid planning)
 
