@@ -185,7 +185,8 @@ typedef struct {
 } vc_cache;
 
 /* Host only.  Workspace bytes viscache_decode_attn needs for caches of at most
- * max_rows rows per (layer, sequence, kv head). */
+ * max_rows rows per (layer, sequence, kv head); 0 if the shape is invalid or
+ * max_rows exceeds 32768. */
 size_t viscache_decode_workspace_bytes(const vc_decode_shape *shape, int64_t max_rows);
 
 /* Device, asynchronous.  Appends one key and one value row per unit
@@ -201,7 +202,8 @@ vc_status viscache_append_kv(const vc_decode_shape *shape, const vc_cache *cache
  * len rows of (l, b, hq / (Hq/Hkv)).  q: DEVICE bf16 [L][B][Hq][d]; out:
  * DEVICE fp32 [L][B][Hq][d]; a cache of length 0 gives zeros.  `workspace`:
  * DEVICE, at least viscache_decode_workspace_bytes(shape, max_rows) bytes,
- * where max_rows bounds every len; 256-byte aligned. */
+ * where max_rows bounds every len (at most 32768, else VC_ERR_UNSUPPORTED);
+ * 256-byte aligned. */
 vc_status viscache_decode_attn(const vc_decode_shape *shape, const vc_cache *cache, const void *q,
                                float *out, float scale, int64_t max_rows, void *workspace,
                                size_t workspace_bytes, void *stream);

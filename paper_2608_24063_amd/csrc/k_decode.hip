@@ -3,11 +3,12 @@
 // query per query head over all cached rows.
 //
 // Attention is split over rows: workgroup = (unit, split of split_rows rows),
-// and each of its four waves takes 32-row tiles in turn.  The G query heads of
+// and each of its four waves takes 32-row tiles in turn, the next tile's rows
+// in flight while the current one is processed.  The G query heads of
 // a kv head form one 16-column MFMA block (heads >= G are zero), so each K/V
 // row is read once for all of them:
 //   S^T = K Q^T   A = K rows straight from HBM, B = Q (registers)
-//   O^T = V^T P^T A = V^T (per-wave transposed LDS tile), B = P^T (registers)
+//   O^T = V^T P^T A = V^T (per-wave LDS tile, transposing reads), B = P^T
 // Partial (max, sum, O) per split go to the workspace; a second kernel merges
 // them in split order.
 #include "vc_device.h"
@@ -44,18 +45,47 @@ __global__ __launch_bounds__(64) void k_append(int32_t units, int32_t d, uint16_
   if (t == 0 && room) stg(len + u, L0 + 1);
 }
 
-__device__ __forceinline__ bf16x8 load_split8(const uint16_t *row, int c) {
-  u32x2 a = *reinterpret_cast<const u32x2 *>(row + c);
-  u32x2 b = *reinterpret_cast<const u32x2 *>(row + c + 16);
-  return as_bf16x8(u32x4{a.x, a.y, b.x, b.y});
+// gfx950 transposing LDS read: within each group of 16 lanes, lane 4a+b gets
+// element b of the 8-byte chunks addressed by lanes a, a+4, a+8 and a+12.
+__device__ __forceinline__ u32x2 lds_read_tr16(const uint16_t *p) {
+  typedef short v4i16 __attribute__((ext_vector_type(4)));
+  const v4i16 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16 *)(p));
+  return __builtin_bit_cast(u32x2, v);
 }
+
+// K and V of one 32-row tile in registers.  K: lane (lr, lg) holds row
+// rb*16 + lr, elements 32 s + 8 lg .. + 7 (the S^T A operand).  V: lane holds
+// 16-byte chunk lane % 16 of rows lane / 16 + 4 it (staged to LDS row-major).
+template <int D>
+struct RowTile {
+  static constexpr int KS = D / 32;
+  static constexpr int kVIt = 32 * D / 8 / 64;  // 16-byte V chunks per lane
+  u32x4 k[2][KS];
+  u32x4 v[kVIt];
+  __device__ __forceinline__ void load(const uint16_t *Kp, const uint16_t *Vp, int t0, int r1, int lr, int lg,
+                                       int lane) {
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+      const int row = min(t0 + rb * 16 + lr, r1 - 1);
+#pragma unroll
+      for (int s = 0; s < KS; ++s) k[rb][s] = ld16(Kp + (int64_t)row * D + 32 * s + 8 * lg);
+    }
+    constexpr int kCpr = D / 8;  // chunks per row
+#pragma unroll
+    for (int it = 0; it < kVIt; ++it) {
+      const int c = lane + 64 * it;
+      const int row = min(t0 + c / kCpr, r1 - 1);
+      v[it] = ld16(Vp + (int64_t)row * D + (c % kCpr) * 8);
+    }
+  }
+};
 
 template <int D>
 __global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
   constexpr int KS = D / 32;
   constexpr int MB = D / 16;
-  constexpr int PT = kRowTile + 8;
-  __shared__ __attribute__((aligned(16))) uint16_t vt[4][D * PT];
+  constexpr int PR = D + 16;  // V tile row pitch: conflict-free transposing reads
+  __shared__ __attribute__((aligned(16))) uint16_t vt[4][kRowTile * PR];
   __shared__ float2 wml[4][16];
   __shared__ __attribute__((aligned(16))) float wo[4][16][D + 4];
 
@@ -92,41 +122,31 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
   float mrow = kFloor, lsum = 0.f;
   const float sc = p.sc;
   uint16_t *myvt = vt[w];
+  const int tr_row = 4 * lg + (lr >> 2), tr_col = 4 * (lr & 3);
 
-  const int ntiles = (r1 - r0 + kRowTile - 1) / kRowTile;
+  // Wave w takes tiles w, w+4, ...; the next tile's rows are in flight while
+  // the current one is processed.
+  const int ntiles = r1 > r0 ? (r1 - r0 + kRowTile - 1) / kRowTile : 0;
+  RowTile<D> cur, nxt;
+  if (w < ntiles) cur.load(Kp, Vp, r0 + w * kRowTile, r1, lr, lg, lane);
   for (int t = w; t < ntiles; t += 4) {
     const int t0 = r0 + t * kRowTile;
-    // K rows -> A operands; S^T for 2 blocks of 16 rows.
+    if (t + 4 < ntiles) nxt.load(Kp, Vp, t0 + 4 * kRowTile, r1, lr, lg, lane);
+    // S^T = K Q^T for 2 blocks of 16 rows.
     f32x4 acc[2];
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
       acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      const int row = t0 + rb * 16 + lr;
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        u32x4 a = {0, 0, 0, 0};
-        if (row < r1) a = ld16(Kp + (int64_t)row * D + 32 * s + 8 * lg);
-        acc[rb] = mfma_bf16(as_bf16x8(a), bq[s], acc[rb]);
-      }
+      for (int s = 0; s < KS; ++s) acc[rb] = mfma_bf16(as_bf16x8(cur.k[rb][s]), bq[s], acc[rb]);
     }
-    // V rows -> transposed per-wave LDS tile [d][32 rows].
+    // V rows -> per-wave LDS tile, row-major (read back transposed below).
     {
-      const int pp = lane & 15;  // rows 2pp, 2pp+1
+      constexpr int kCpr = D / 8;
 #pragma unroll
-      for (int it = 0; it < D / 32; ++it) {
-        const int c = (lane >> 4) + 4 * it;  // 16-byte chunk of the row
-        const int ra = t0 + 2 * pp, rb2 = ra + 1;
-        u32x4 va = {0, 0, 0, 0}, vb = {0, 0, 0, 0};
-        if (ra < r1) va = ld16(Vp + (int64_t)ra * D + c * 8);
-        if (rb2 < r1) vb = ld16(Vp + (int64_t)rb2 * D + c * 8);
-        const uint32_t ea[4] = {va.x, va.y, va.z, va.w}, eb[4] = {vb.x, vb.y, vb.z, vb.w};
-#pragma unroll
-        for (int qq = 0; qq < 4; ++qq) {
-          uint32_t lo = (ea[qq] & 0xFFFFu) | (eb[qq] << 16);
-          uint32_t hi = (ea[qq] >> 16) | (eb[qq] & 0xFFFF0000u);
-          *reinterpret_cast<uint32_t *>(myvt + (c * 8 + 2 * qq) * PT + 2 * pp) = lo;
-          *reinterpret_cast<uint32_t *>(myvt + (c * 8 + 2 * qq + 1) * PT + 2 * pp) = hi;
-        }
+      for (int it = 0; it < RowTile<D>::kVIt; ++it) {
+        const int c = lane + 64 * it;
+        *reinterpret_cast<u32x4 *>(myvt + (c / kCpr) * PR + (c % kCpr) * 8) = cur.v[it];
       }
     }
     // Online softmax per head (lane column); lane groups share the max.
@@ -163,13 +183,18 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
                       pack_bf16(pr[1][2] - bf16_lo(hi.w), pr[1][3] - bf16_hi(hi.w))};
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes landed
     __builtin_amdgcn_wave_barrier();
+    // O^T += V^T P^T: A = V^T (16 d x 32 rows) from transposing reads.
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
-      const bf16x8 a = load_split8(myvt + (mb * 16 + lr) * PT, 4 * lg);
+      const uint16_t *base = myvt + tr_row * PR + 16 * mb + tr_col;
+      const u32x2 lo4 = lds_read_tr16(base), hi4 = lds_read_tr16(base + 16 * PR);
+      const bf16x8 a = as_bf16x8(u32x4{lo4.x, lo4.y, hi4.x, hi4.y});
       O[mb] = mfma_bf16(a, as_bf16x8(hi), O[mb]);
       O[mb] = mfma_bf16(a, as_bf16x8(lo), O[mb]);
     }
-    __builtin_amdgcn_wave_barrier();  // reads done before the next tile's writes
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the next tile's writes
+    __builtin_amdgcn_wave_barrier();
+    cur = nxt;
   }
 
   // Merge the four waves, then store this split's partial.
@@ -205,6 +230,7 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
 }
 
 // Merge split partials in split order; out = O / sum (zeros for empty caches).
+// Every partial of an output element is loaded in one batch.
 template <int D>
 __global__ __launch_bounds__(256) void k_decode_combine(DecodePlan p) {
   const int u = blockIdx.x;
@@ -212,20 +238,27 @@ __global__ __launch_bounds__(256) void k_decode_combine(DecodePlan p) {
   const int ns = len > 0 ? min(p.nsplit, (len + p.split_rows - 1) / p.split_rows) : 1;
   const int g = u % p.Hkv;
   const int lb_ = u / p.Hkv;
-  const float sc = p.sc;
   for (int e = threadIdx.x; e < p.G * D; e += 256) {
     const int h = e / D, x = e % D;
+    float2 ml[kMaxDecodeSplits];
+    float po[kMaxDecodeSplits];
+#pragma unroll
+    for (int s = 0; s < kMaxDecodeSplits; ++s) {
+      const int64_t pb = ((int64_t)u * p.nsplit + s) * 16 + h;
+      ml[s] = s < ns ? ldg(p.part_ml + pb) : make_float2(kNegInf, 0.f);
+      po[s] = s < ns ? ldg(p.part_o + pb * D + x) : 0.f;
+    }
     float M = kNegInf;
-    for (int s = 0; s < ns; ++s) M = fmaxf(M, ldg(p.part_ml + ((int64_t)u * p.nsplit + s) * 16 + h).x);
+#pragma unroll
+    for (int s = 0; s < kMaxDecodeSplits; ++s) M = fmaxf(M, ml[s].x);
     float o = 0.f, sum = 0.f;
     if (M != kNegInf) {
-      for (int s = 0; s < ns; ++s) {
-        const int64_t pb = ((int64_t)u * p.nsplit + s) * 16 + h;
-        const float2 ml = ldg(p.part_ml + pb);
-        if (ml.x == kNegInf) continue;
-        const float f = fast_exp2(ml.x - M);
-        o += f * ldg(p.part_o + pb * D + x);
-        sum += f * ml.y;
+#pragma unroll
+      for (int s = 0; s < kMaxDecodeSplits; ++s) {
+        if (ml[s].x == kNegInf) continue;
+        const float f = fast_exp2(ml[s].x - M);
+        o += f * po[s];
+        sum += f * ml[s].y;
       }
     }
     stg(p.out + ((int64_t)lb_ * p.Hq + (int64_t)g * p.G + h) * D + x, sum > 0.f ? o / sum : 0.f);

@@ -378,7 +378,6 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
 // ---- decode ----------------------------------------------------------------
 
 namespace {
-constexpr int32_t kSplitRows = 512;
 
 vc_status check_decode(const vc_decode_shape *s) {
   if (!s) return VC_ERR_ARG;
@@ -390,12 +389,13 @@ vc_status check_decode(const vc_decode_shape *s) {
 }
 
 int32_t decode_splits(int64_t max_rows) {
-  return (int32_t)std::max<int64_t>(1, (max_rows + kSplitRows - 1) / kSplitRows);
+  return (int32_t)std::max<int64_t>(1, (max_rows + kDecodeSplitRows - 1) / kDecodeSplitRows);
 }
 }  // namespace
 
 size_t viscache_decode_workspace_bytes(const vc_decode_shape *s, int64_t max_rows) {
   if (check_decode(s) != VC_OK || max_rows < 0) return 0;
+  if (max_rows > (int64_t)kDecodeSplitRows * kMaxDecodeSplits) return 0;
   const int64_t units = (int64_t)s->L * s->B * s->Hkv;
   const int64_t ns = decode_splits(max_rows);
   return align_up(sizeof(float) * (size_t)(units * ns * 16 * s->d)) +
@@ -423,6 +423,7 @@ vc_status viscache_decode_attn(const vc_decode_shape *s, const vc_cache *c, cons
   if (st != VC_OK) return st;
   if (!c || !c->k_pool || !c->v_pool || !c->row_off || !c->cap || !c->len || !q || !out) return VC_ERR_ARG;
   if (!(scale > 0.f) || !std::isfinite(scale) || max_rows < 0) return VC_ERR_ARG;
+  if (max_rows > (int64_t)kDecodeSplitRows * kMaxDecodeSplits) return VC_ERR_UNSUPPORTED;
   const size_t need = viscache_decode_workspace_bytes(s, max_rows);
   if (!workspace || workspace_bytes < need) return VC_ERR_WORKSPACE;
   if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return VC_ERR_WORKSPACE;
@@ -430,7 +431,7 @@ vc_status viscache_decode_attn(const vc_decode_shape *s, const vc_cache *c, cons
   DecodePlan p{};
   p.B = s->B; p.L = s->L; p.Hq = s->Hq; p.Hkv = s->Hkv; p.d = s->d; p.G = s->Hq / s->Hkv;
   p.nsplit = decode_splits(max_rows);
-  p.split_rows = kSplitRows;
+  p.split_rows = kDecodeSplitRows;
   p.sc = scale * 1.4426950408889634f;
   p.k_pool = static_cast<const uint16_t *>(c->k_pool);
   p.v_pool = static_cast<const uint16_t *>(c->v_pool);

@@ -78,6 +78,9 @@ hipError_t launch_score_global(const PrunePlan &p, hipStream_t st);
 hipError_t launch_select(const PrunePlan &p, hipStream_t st);
 hipError_t launch_fuse(const PrunePlan &p, hipStream_t st);
 
+constexpr int kDecodeSplitRows = 1024;  // cache rows per decode workgroup
+constexpr int kMaxDecodeSplits = 32;    // => at most 32768 cached rows per unit
+
 struct DecodePlan {
   int32_t B, L, Hq, Hkv, d, G;
   int32_t nsplit;    // row splits per unit

@@ -147,3 +147,15 @@ def test_decode_rejects_bad_arguments(vc):
     with pytest.raises(vc.VisCacheError) as ei:
         vc.viscache_append_kv(ds, vc.vc_cache(0, 256, 256, 256, 256), 256, 256, 0)
     assert ei.value.status == vc.VC_ERR_ARG
+
+
+def test_decode_row_limit(vc):
+    """Caches longer than 32 splits of 1024 rows are refused on the host."""
+    ds = vc.vc_decode_shape(1, 2, 8, 2, 128)
+    assert vc.viscache_decode_workspace_bytes(ds, 32768) > 0
+    assert vc.viscache_decode_workspace_bytes(ds, 32769) == 0
+    c = vc.vc_cache(256, 256, 256, 256, 256)
+    need = vc.viscache_decode_workspace_bytes(ds, 32768)
+    with pytest.raises(vc.VisCacheError) as ei:
+        vc.viscache_decode_attn(ds, c, 256, 256, 0.1, 32769, 256, need, 0)
+    assert ei.value.status == vc.VC_ERR_UNSUPPORTED

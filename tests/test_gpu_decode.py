@@ -37,7 +37,9 @@ def test_decode_random_caches(dev, orc, sg, d, Hq, Hkv):
     from synthgen.device import bf16_tensor, to_host_bf16
     L, B = 2, 2
     units = L * B * Hkv
-    lens = [0, 1, 31, 33, 100, 511, 512, 513, 1100, 5, 64, 700, 2, 1025, 47, 256][:units]
+    # Empty, sub-tile, tile edges, split edges (1024 rows per split) and
+    # several splits.
+    lens = [0, 1, 31, 33, 3100, 511, 1023, 1024, 1100, 5, 64, 2049, 2, 1025, 47, 4097][:units]
     lens += [17] * (units - len(lens))
     caps = [x + 3 for x in lens]
     c = DecodeCache(L, B, Hq, Hkv, d, caps, dev)
