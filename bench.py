@@ -299,8 +299,7 @@ def decode_latency(w, pc, dev, steps, flush_buf, torch, sg):
             if flush_buf is not None:
                 flush_buf.sum()
             ev[t][0].record()
-            c.append(kn[t], vn[t])
-            c.attend(q[t], out, d ** -0.5)
+            c.step(kn[t], vn[t], q[t], out, d ** -0.5)  # append + attend, one launch
             ev[t][1].record()
         torch.cuda.synchronize()
         ts = sorted(a.elapsed_time(b) * 1e3 for a, b in ev)

@@ -208,6 +208,25 @@ vc_status viscache_decode_attn(const vc_decode_shape *shape, const vc_cache *cac
                                float *out, float scale, int64_t max_rows, void *workspace,
                                size_t workspace_bytes, void *stream);
 
+/* Host only.  Workspace bytes viscache_decode_step needs (the decode
+ * workspace plus one arrival counter per unit); 0 if the shape is invalid or
+ * max_rows exceeds 32768. */
+size_t viscache_decode_step_workspace_bytes(const vc_decode_shape *shape, int64_t max_rows);
+
+/* Device, asynchronous.  One decode step in a single launch, with the result
+ * of viscache_append_kv followed by viscache_decode_attn (Sec. 2, decoding):
+ * the new K/V row of every unit (k_new, v_new: DEVICE bf16 [L][B][Hkv][d]) is
+ * appended where there is room and attended together with the cached rows;
+ * q, out, scale and max_rows as for viscache_decode_attn (max_rows also
+ * bounds the length after the append).  `workspace`: DEVICE, at least
+ * viscache_decode_step_workspace_bytes(shape, max_rows) bytes, 256-byte
+ * aligned, zero-filled before its first use and not modified by the caller
+ * between calls (the call leaves its counters at zero).  Calls sharing a
+ * workspace must be ordered on one stream. */
+vc_status viscache_decode_step(const vc_decode_shape *shape, const vc_cache *cache, const void *k_new,
+                               const void *v_new, const void *q, float *out, float scale,
+                               int64_t max_rows, void *workspace, size_t workspace_bytes, void *stream);
+
 /* Static text for a status code. */
 const char *viscache_strerror(vc_status s);
 

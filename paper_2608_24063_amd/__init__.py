@@ -76,11 +76,15 @@ def lib() -> ctypes.CDLL:
         L.viscache_append_kv.argtypes = [P(vc_decode_shape), P(vc_cache), c_vp, c_vp, c_vp]
         L.viscache_decode_attn.argtypes = [P(vc_decode_shape), P(vc_cache), c_vp, c_vp, c_f32, c_i64,
                                            c_vp, ctypes.c_size_t, c_vp]
+        L.viscache_decode_step_workspace_bytes.argtypes = [P(vc_decode_shape), c_i64]
+        L.viscache_decode_step_workspace_bytes.restype = ctypes.c_size_t
+        L.viscache_decode_step.argtypes = [P(vc_decode_shape), P(vc_cache), c_vp, c_vp, c_vp, c_vp, c_f32,
+                                           c_i64, c_vp, ctypes.c_size_t, c_vp]
         L.viscache_strerror.argtypes = [c_i32]
         L.viscache_strerror.restype = ctypes.c_char_p
         for name in ("viscache_budget", "viscache_out_rows", "viscache_prune", "viscache_prune_score_offsets",
                      "viscache_prune_staged",
-                     "viscache_append_kv", "viscache_decode_attn"):
+                     "viscache_append_kv", "viscache_decode_attn", "viscache_decode_step"):
             getattr(L, name).restype = c_i32
         _lib = L
     return _lib
@@ -190,6 +194,17 @@ def viscache_decode_attn(shape: vc_decode_shape, cache: vc_cache, q: int, out: i
                                       workspace, workspace_bytes, stream), "viscache_decode_attn")
 
 
+def viscache_decode_step_workspace_bytes(shape: vc_decode_shape, max_rows: int) -> int:
+    return int(lib().viscache_decode_step_workspace_bytes(ctypes.byref(shape), max_rows))
+
+
+def viscache_decode_step(shape: vc_decode_shape, cache: vc_cache, k_new: int, v_new: int, q: int, out: int,
+                         scale: float, max_rows: int, workspace: int, workspace_bytes: int,
+                         stream: int) -> None:
+    _check(lib().viscache_decode_step(ctypes.byref(shape), ctypes.byref(cache), k_new, v_new, q, out, scale,
+                                      max_rows, workspace, workspace_bytes, stream), "viscache_decode_step")
+
+
 def viscache_strerror(status: int) -> str:
     return strerror(status)
 
@@ -197,4 +212,5 @@ def viscache_strerror(status: int) -> str:
 EXPORTED = ("viscache_default_params", "viscache_budget", "viscache_out_rows",
             "viscache_prune_workspace_bytes", "viscache_prune_score_offsets", "viscache_prune",
             "viscache_prune_staged", "viscache_decode_workspace_bytes",
-            "viscache_append_kv", "viscache_decode_attn", "viscache_strerror")
+            "viscache_append_kv", "viscache_decode_attn", "viscache_decode_step_workspace_bytes",
+            "viscache_decode_step", "viscache_strerror")

@@ -62,40 +62,68 @@ struct RowTile {
   static constexpr int kVIt = 32 * D / 8 / 64;  // 16-byte V chunks per lane
   u32x4 k[2][KS];
   u32x4 v[kVIt];
+  // Row `nrow` (if >= 0) is not in the pool yet: it comes from knew / vnew.
   __device__ __forceinline__ void load(const uint16_t *Kp, const uint16_t *Vp, int t0, int r1, int lr, int lg,
-                                       int lane) {
+                                       int lane, int nrow, const uint16_t *knew, const uint16_t *vnew) {
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
       const int row = min(t0 + rb * 16 + lr, r1 - 1);
+      const uint16_t *src = row == nrow ? knew : Kp + (int64_t)row * D;
 #pragma unroll
-      for (int s = 0; s < KS; ++s) k[rb][s] = ld16(Kp + (int64_t)row * D + 32 * s + 8 * lg);
+      for (int s = 0; s < KS; ++s) k[rb][s] = ld16(src + 32 * s + 8 * lg);
     }
     constexpr int kCpr = D / 8;  // chunks per row
 #pragma unroll
     for (int it = 0; it < kVIt; ++it) {
       const int c = lane + 64 * it;
       const int row = min(t0 + c / kCpr, r1 - 1);
-      v[it] = ld16(Vp + (int64_t)row * D + (c % kCpr) * 8);
+      const uint16_t *src = row == nrow ? vnew : Vp + (int64_t)row * D;
+      v[it] = ld16(src + (c % kCpr) * 8);
     }
   }
 };
 
+// Partials of the fused step are exchanged between workgroups that may sit
+// on different XCDs (separate L2s): they are written and read with
+// device-coherent accesses instead of fences that would write back and
+// invalidate a whole L2.
+template <bool COHERENT>
+__device__ __forceinline__ void st_part(float *p, float v) {
+  if (COHERENT)
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else
+    stg(p, v);
+}
+template <bool COHERENT>
+__device__ __forceinline__ float ld_part(const float *p) {
+  if (COHERENT) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return ldg(p);
+}
+
 template <int D>
-__global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
+struct DecodeSmem {
+  static constexpr int PR = D + 16;  // V tile row pitch: conflict-free transposing reads
+  uint16_t vt[4][kRowTile * PR] __attribute__((aligned(16)));
+  float2 wml[4][16];
+  float wo[4][16][D + 4] __attribute__((aligned(16)));
+  uint32_t last;
+};
+
+// Attention of the query heads of unit u over cache rows [r0, r1) (row nrow,
+// if >= 0, read from knew / vnew); writes the split's partial (max, sum, O).
+// Where a split's result goes: its partial (plain or device-coherent stores),
+// or, for a unit with a single split, the normalised output itself.
+enum SplitOut { kPartial = 0, kPartialCoherent = 1, kOutput = 2 };
+
+template <int D, int OUT>
+__device__ __forceinline__ void attend_split(const DecodePlan &p, DecodeSmem<D> &sm, int u, int split, int r0,
+                                             int r1, int nrow, const uint16_t *knew, const uint16_t *vnew) {
   constexpr int KS = D / 32;
   constexpr int MB = D / 16;
-  constexpr int PR = D + 16;  // V tile row pitch: conflict-free transposing reads
-  __shared__ __attribute__((aligned(16))) uint16_t vt[4][kRowTile * PR];
-  __shared__ float2 wml[4][16];
-  __shared__ __attribute__((aligned(16))) float wo[4][16][D + 4];
-
-  const uint32_t lb = xcd_block(blockIdx.x, gridDim.x);
-  const int split = lb % p.nsplit;
-  const int u = lb / p.nsplit;
-  const int len = min(ldg(p.len + u), ldg(p.cap + u));
-  const int r0 = split * p.split_rows;
-  if (r0 >= len && split > 0) return;  // uniform: nothing for this split
-  const int r1 = min(len, r0 + p.split_rows);
+  constexpr int PR = DecodeSmem<D>::PR;
+  auto &vt = sm.vt;
+  auto &wml = sm.wml;
+  auto &wo = sm.wo;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int g = u % p.Hkv;
@@ -128,10 +156,10 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
   // the current one is processed.
   const int ntiles = r1 > r0 ? (r1 - r0 + kRowTile - 1) / kRowTile : 0;
   RowTile<D> cur, nxt;
-  if (w < ntiles) cur.load(Kp, Vp, r0 + w * kRowTile, r1, lr, lg, lane);
+  if (w < ntiles) cur.load(Kp, Vp, r0 + w * kRowTile, r1, lr, lg, lane, nrow, knew, vnew);
   for (int t = w; t < ntiles; t += 4) {
     const int t0 = r0 + t * kRowTile;
-    if (t + 4 < ntiles) nxt.load(Kp, Vp, t0 + 4 * kRowTile, r1, lr, lg, lane);
+    if (t + 4 < ntiles) nxt.load(Kp, Vp, t0 + 4 * kRowTile, r1, lr, lg, lane, nrow, knew, vnew);
     // S^T = K Q^T for 2 blocks of 16 rows.
     f32x4 acc[2];
 #pragma unroll
@@ -224,18 +252,37 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
         }
       }
     }
-    stg(p.part_o + (pbase + h) * D + x, o);
-    if (x == 0) stg(p.part_ml + pbase + h, make_float2(M, s));
+    if (OUT == kOutput) {
+      // The merge of a single split: its factor is exp2(0) = 1 exactly.
+      if (h < p.G) stg(p.out + ((int64_t)lb_ * p.Hq + (int64_t)g * p.G + h) * D + x, s > 0.f ? o / s : 0.f);
+      continue;
+    }
+    st_part<OUT == kPartialCoherent>(p.part_o + (pbase + h) * D + x, o);
+    if (x == 0) {
+      float *ml = reinterpret_cast<float *>(p.part_ml + pbase + h);
+      st_part<OUT == kPartialCoherent>(ml, M);
+      st_part<OUT == kPartialCoherent>(ml + 1, s);
+    }
   }
 }
 
-// Merge split partials in split order; out = O / sum (zeros for empty caches).
-// Every partial of an output element is loaded in one batch.
 template <int D>
-__global__ __launch_bounds__(256) void k_decode_combine(DecodePlan p) {
-  const int u = blockIdx.x;
+__global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
+  __shared__ DecodeSmem<D> sm;
+  const uint32_t lb = xcd_block(blockIdx.x, gridDim.x);
+  const int split = lb % p.nsplit;
+  const int u = lb / p.nsplit;
   const int len = min(ldg(p.len + u), ldg(p.cap + u));
-  const int ns = len > 0 ? min(p.nsplit, (len + p.split_rows - 1) / p.split_rows) : 1;
+  const int r0 = split * p.split_rows;
+  if (r0 >= len && split > 0) return;  // uniform: nothing for this split
+  attend_split<D, kPartial>(p, sm, u, split, r0, min(len, r0 + p.split_rows), -1, nullptr, nullptr);
+}
+
+// Merge the split partials of unit u in split order; out = O / sum (zeros
+// for an empty cache).  Every partial of an output element is loaded in one
+// batch.
+template <int D, bool COHERENT>
+__device__ __forceinline__ void merge_splits(const DecodePlan &p, int u, int ns) {
   const int g = u % p.Hkv;
   const int lb_ = u / p.Hkv;
   for (int e = threadIdx.x; e < p.G * D; e += 256) {
@@ -245,8 +292,9 @@ __global__ __launch_bounds__(256) void k_decode_combine(DecodePlan p) {
 #pragma unroll
     for (int s = 0; s < kMaxDecodeSplits; ++s) {
       const int64_t pb = ((int64_t)u * p.nsplit + s) * 16 + h;
-      ml[s] = s < ns ? ldg(p.part_ml + pb) : make_float2(kNegInf, 0.f);
-      po[s] = s < ns ? ldg(p.part_o + pb * D + x) : 0.f;
+      const float *mlp = reinterpret_cast<const float *>(p.part_ml + pb);
+      ml[s] = s < ns ? make_float2(ld_part<COHERENT>(mlp), ld_part<COHERENT>(mlp + 1)) : make_float2(kNegInf, 0.f);
+      po[s] = s < ns ? ld_part<COHERENT>(p.part_o + pb * D + x) : 0.f;
     }
     float M = kNegInf;
 #pragma unroll
@@ -265,6 +313,68 @@ __global__ __launch_bounds__(256) void k_decode_combine(DecodePlan p) {
   }
 }
 
+// One decode step in one launch: append (the split holding the new row takes
+// it from k_new / v_new and writes it to the pool), attention per split, and
+// the merge done by the last split of each unit to arrive, which also
+// advances len and re-arms the unit's counter.
+template <int D>
+__global__ __launch_bounds__(256, 2) void k_decode_step(DecodePlan p) {
+  __shared__ DecodeSmem<D> sm;
+  const uint32_t lb = xcd_block(blockIdx.x, gridDim.x);
+  const int split = lb % p.nsplit;
+  const int u = lb / p.nsplit;
+  const int len0 = ldg(p.len + u), cap = ldg(p.cap + u);
+  const bool room = len0 < cap;
+  const int len = room ? len0 + 1 : min(len0, cap);  // rows attended this step
+  // Rows past nsplit * split_rows (a length beyond max_rows) are not attended.
+  const int ns = min(p.nsplit, max(1, (len + p.split_rows - 1) / p.split_rows));
+  // Every launched split of the unit arrives at the counter below, so every
+  // read of len above happens before the last arriver advances it.
+  if (split < ns) {  // uniform
+    const int r0 = split * p.split_rows, r1 = min(len, r0 + p.split_rows);
+    const int nrow = room ? len0 : -1;
+    const uint16_t *knew = p.k_new + (int64_t)u * D, *vnew = p.v_new + (int64_t)u * D;
+    if (room && nrow >= r0 && nrow < r1 && threadIdx.x < 2 * (D / 8)) {
+      const int c = threadIdx.x, cc = c % (D / 8);
+      const int64_t dst = (ldg(p.row_off + u) + nrow) * D + cc * 8;
+      if (c < D / 8)
+        st16(p.k_pool_w + dst, ld16(knew + cc * 8));
+      else
+        st16(p.v_pool_w + dst, ld16(vnew + cc * 8));
+    }
+    if (ns == 1)
+      attend_split<D, kOutput>(p, sm, u, split, r0, r1, nrow, knew, vnew);
+    else
+      attend_split<D, kPartialCoherent>(p, sm, u, split, r0, r1, nrow, knew, vnew);
+  }
+  if (p.nsplit == 1) {  // the only workgroup of the unit: nothing to merge or count
+    if (threadIdx.x == 0 && room) stg(p.len_w + u, len);
+    return;
+  }
+  // The partial's device-coherent stores complete before the arrival is
+  // counted; the last arriver reads every partial with device-coherent loads.
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0)
+    sm.last = __hip_atomic_fetch_add(p.arrive + u, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+              (uint32_t)(p.nsplit - 1);
+  __syncthreads();
+  if (!sm.last) return;
+  if (ns > 1) merge_splits<D, true>(p, u, ns);
+  if (threadIdx.x == 0) {
+    __hip_atomic_store(p.arrive + u, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (room) stg(p.len_w + u, len);
+  }
+}
+
+// Merge split partials of each unit (second kernel of the two-call path).
+template <int D>
+__global__ __launch_bounds__(256) void k_decode_combine(DecodePlan p) {
+  const int u = blockIdx.x;
+  const int len = min(ldg(p.len + u), ldg(p.cap + u));
+  merge_splits<D, false>(p, u, len > 0 ? min(p.nsplit, (len + p.split_rows - 1) / p.split_rows) : 1);
+}
+
 }  // namespace
 
 hipError_t launch_append(int32_t units, int32_t d, uint16_t *k_pool, uint16_t *v_pool,
@@ -273,6 +383,17 @@ hipError_t launch_append(int32_t units, int32_t d, uint16_t *k_pool, uint16_t *v
   if (units == 0) return hipSuccess;
   hipLaunchKernelGGL(k_append, dim3(units), dim3(64), 0, st, units, d, k_pool, v_pool, row_off,
                      cap, len, k_new, v_new);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_step(const DecodePlan &p, hipStream_t st) {
+  const int units = p.L * p.B * p.Hkv;
+  if (units == 0) return hipSuccess;
+  const uint32_t grid = (uint32_t)units * p.nsplit;
+  if (p.d == 128)
+    hipLaunchKernelGGL(k_decode_step<128>, dim3(grid), dim3(256), 0, st, p);
+  else
+    hipLaunchKernelGGL(k_decode_step<64>, dim3(grid), dim3(256), 0, st, p);
   return hipGetLastError();
 }
 

@@ -78,7 +78,7 @@ hipError_t launch_score_global(const PrunePlan &p, hipStream_t st);
 hipError_t launch_select(const PrunePlan &p, hipStream_t st);
 hipError_t launch_fuse(const PrunePlan &p, hipStream_t st);
 
-constexpr int kDecodeSplitRows = 1024;  // cache rows per decode workgroup
+constexpr int kDecodeSplitRows = 1024;  // most cache rows per decode workgroup
 constexpr int kMaxDecodeSplits = 32;    // => at most 32768 cached rows per unit
 
 struct DecodePlan {
@@ -94,11 +94,18 @@ struct DecodePlan {
   float *out;
   float *part_o;     // [U][nsplit][16][d]
   float2 *part_ml;   // [U][nsplit][16]
+  // Fused step only: the row to append per unit ([U][d] each), the arrival
+  // counters of the split merge, and the writable views of pools and lengths.
+  const uint16_t *k_new, *v_new;
+  uint32_t *arrive;  // [U], zero between calls
+  uint16_t *k_pool_w, *v_pool_w;
+  int32_t *len_w;
 };
 
 hipError_t launch_append(int32_t units, int32_t d, uint16_t *k_pool, uint16_t *v_pool,
                          const int64_t *row_off, const int32_t *cap, int32_t *len,
                          const uint16_t *k_new, const uint16_t *v_new, hipStream_t st);
 hipError_t launch_decode(const DecodePlan &p, hipStream_t st);
+hipError_t launch_decode_step(const DecodePlan &p, hipStream_t st);
 
 }  // namespace vc

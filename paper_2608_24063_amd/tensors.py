@@ -6,7 +6,8 @@ from __future__ import annotations
 import torch
 
 from . import (VC_PRUNE_EVENTS, VC_RANK_GLOBAL, make_params, make_shape, vc_cache, vc_decode_shape,
-               viscache_append_kv, viscache_budget, viscache_decode_attn, viscache_decode_workspace_bytes,
+               viscache_append_kv, viscache_budget, viscache_decode_attn, viscache_decode_step,
+               viscache_decode_step_workspace_bytes, viscache_decode_workspace_bytes,
                viscache_out_rows, viscache_prune, viscache_prune_staged, viscache_prune_workspace_bytes)
 
 
@@ -111,6 +112,9 @@ class DecodeCache:
         self.offs_host, self.caps_host = offs, caps
         self.ws_bytes = viscache_decode_workspace_bytes(self.shape, self.max_cap)
         self.ws = torch.empty((max(self.ws_bytes, 256),), dtype=torch.uint8, device=device)
+        # The fused step keeps arrival counters in its workspace: zero-filled once.
+        self.step_ws_bytes = viscache_decode_step_workspace_bytes(self.shape, self.max_cap)
+        self.step_ws = torch.zeros((max(self.step_ws_bytes, 256),), dtype=torch.uint8, device=device)
         self.c = vc_cache(self.k_pool.data_ptr(), self.v_pool.data_ptr(), self.row_off.data_ptr(),
                           self.cap.data_ptr(), self.len.data_ptr())
 
@@ -120,6 +124,13 @@ class DecodeCache:
     def attend(self, q: torch.Tensor, out: torch.Tensor, scale: float) -> None:
         viscache_decode_attn(self.shape, self.c, q.data_ptr(), out.data_ptr(), scale, self.max_cap,
                              self.ws.data_ptr(), self.ws_bytes, _stream())
+
+    def step(self, k_new: torch.Tensor, v_new: torch.Tensor, q: torch.Tensor, out: torch.Tensor,
+             scale: float) -> None:
+        """append + attend in one launch (viscache_decode_step)."""
+        viscache_decode_step(self.shape, self.c, k_new.data_ptr(), v_new.data_ptr(), q.data_ptr(),
+                             out.data_ptr(), scale, self.max_cap, self.step_ws.data_ptr(), self.step_ws_bytes,
+                             _stream())
 
 
 __all__ = ["PruneCall", "DecodeCache", "make_params"]

@@ -150,3 +150,62 @@ def test_decode_over_pruned_cache(dev, orc, sg):
                         h = g * w.G + hh
                         _check_out(orc, q[l, b, h], K[r0:r0 + ln[u]], V[r0:r0 + ln[u]], o[l, b, h], scale,
                                    f"step {t} l={l} h={h}")
+
+
+@pytest.mark.parametrize("d,Hq,Hkv", [(128, 28, 4), (64, 8, 2)])
+def test_decode_step_matches_append_then_attend(dev, orc, sg, d, Hq, Hkv):
+    """viscache_decode_step (one launch) against viscache_append_kv followed by
+    viscache_decode_attn on a copy of the same cache, over several steps:
+    identical outputs (bit for bit), lengths and pools; the oracle checks the
+    attention.  Lengths cross tile and split edges and reach capacity."""
+    from paper_2608_24063_amd.tensors import DecodeCache
+    from synthgen.device import bf16_tensor, to_host_bf16
+    L, B = 2, 1
+    units = L * B * Hkv
+    lens = [0, 1022, 1023, 31, 2047, 5, 64, 3000][:units]
+    caps = [x + 4 for x in lens]
+    caps[1] = lens[1] + 2  # reaches capacity after two appends
+    a = DecodeCache(L, B, Hq, Hkv, d, caps, dev)
+    c = DecodeCache(L, B, Hq, Hkv, d, caps, dev)
+    Kp = _bits(sg, 21, 1, (a.total_rows, d))
+    Vp = _bits(sg, 21, 2, (a.total_rows, d))
+    for cc in (a, c):
+        cc.k_pool.copy_(bf16_tensor(Kp, dev))
+        cc.v_pool.copy_(bf16_tensor(Vp, dev))
+        cc.len.copy_(torch.tensor(lens, dtype=torch.int32))
+    scale = d ** -0.5
+    cur = list(lens)
+    for t in range(4):
+        kn = _bits(sg, 22 + t, 1, (L, B, Hkv, d))
+        vn = _bits(sg, 22 + t, 2, (L, B, Hkv, d))
+        q = _bits(sg, 22 + t, 3, (L, B, Hq, d))
+        kt, vt, qt = bf16_tensor(kn, dev), bf16_tensor(vn, dev), bf16_tensor(q, dev)
+        out_a = torch.full((L, B, Hq, d), float("nan"), dtype=torch.float32, device=dev)
+        out_c = torch.full((L, B, Hq, d), float("nan"), dtype=torch.float32, device=dev)
+        a.append(kt, vt)
+        a.attend(qt, out_a, scale)
+        c.step(kt, vt, qt, out_c, scale)
+        torch.cuda.synchronize()
+        assert torch.equal(out_a, out_c), f"step {t}: fused step differs from append + attend"
+        assert a.len.cpu().tolist() == c.len.cpu().tolist()
+        cur = [min(x + 1, cap) for x, cap in zip(cur, caps)]
+        assert c.len.cpu().tolist() == cur
+        assert torch.equal(a.k_pool, c.k_pool) and torch.equal(a.v_pool, c.v_pool)
+    # The oracle on the final step.
+    K = to_host_bf16(c.k_pool)
+    V = to_host_bf16(c.v_pool)
+    o = out_c.cpu().numpy()
+    G = Hq // Hkv
+    for l in range(L):
+        for b in range(B):
+            for g in range(Hkv):
+                u = (l * B + b) * Hkv + g
+                r0, n = c.offs_host[u], cur[u]
+                for hh in range(0, G, 3):
+                    h = g * G + hh
+                    _check_out(orc, q[l, b, h], K[r0:r0 + n], V[r0:r0 + n], o[l, b, h], scale,
+                               f"step l={l} g={g} h={h} n={n}")
+    # The arrival counters (after the decode partials) are back at zero.
+    import paper_2608_24063_amd as vc
+    base = vc.viscache_decode_workspace_bytes(c.shape, c.max_cap)
+    assert int(c.step_ws[base:base + 4 * units].view(torch.int32).abs().sum()) == 0
