@@ -186,7 +186,8 @@ typedef struct {
 
 /* Host only.  Workspace bytes viscache_decode_attn needs for caches of at most
  * max_rows rows per (layer, sequence, kv head); 0 if the shape is invalid or
- * max_rows exceeds 32768. */
+ * max_rows is negative or so large that L*B*Hkv*ceil(max_rows/32) reaches
+ * 2^31. */
 size_t viscache_decode_workspace_bytes(const vc_decode_shape *shape, int64_t max_rows);
 
 /* Device, asynchronous.  Appends one key and one value row per unit
@@ -202,15 +203,20 @@ vc_status viscache_append_kv(const vc_decode_shape *shape, const vc_cache *cache
  * len rows of (l, b, hq / (Hq/Hkv)).  q: DEVICE bf16 [L][B][Hq][d]; out:
  * DEVICE fp32 [L][B][Hq][d]; a cache of length 0 gives zeros.  `workspace`:
  * DEVICE, at least viscache_decode_workspace_bytes(shape, max_rows) bytes,
- * where max_rows bounds every len (at most 32768, else VC_ERR_UNSUPPORTED);
- * 256-byte aligned. */
+ * where max_rows bounds every len (rows past max_rows are not attended;
+ * VC_ERR_UNSUPPORTED where the workspace size is 0); 256-byte aligned.  Work
+ * is balanced over capacities: each unit's cap rows (at most max_rows) are
+ * cut into pieces of nearly equal size, their number in proportion to cap,
+ * one workgroup each, so a cache whose units differ widely in length
+ * still fills the chip when cap tracks len.  Where a unit's rows are cut
+ * changes its result only by rounding. */
 vc_status viscache_decode_attn(const vc_decode_shape *shape, const vc_cache *cache, const void *q,
                                float *out, float scale, int64_t max_rows, void *workspace,
                                size_t workspace_bytes, void *stream);
 
 /* Host only.  Workspace bytes viscache_decode_step needs (the decode
- * workspace plus one arrival counter per unit); 0 if the shape is invalid or
- * max_rows exceeds 32768. */
+ * workspace plus one arrival counter per unit); 0 where
+ * viscache_decode_workspace_bytes is 0. */
 size_t viscache_decode_step_workspace_bytes(const vc_decode_shape *shape, int64_t max_rows);
 
 /* Device, asynchronous.  One decode step in a single launch, with the result

@@ -2,15 +2,21 @@
 // Decoding"): append one K/V row per (layer, sequence, kv head) and attend one
 // query per query head over all cached rows.
 //
-// Attention is split over rows: workgroup = (unit, split of split_rows rows),
-// and each of its four waves takes 32-row tiles in turn, the next tile's rows
-// in flight while the current one is processed.  The G query heads of
-// a kv head form one 16-column MFMA block (heads >= G are zero), so each K/V
-// row is read once for all of them:
+// Work is balanced over rows, not units: the 32-row tiles of every unit's
+// capacity are split into pieces of nearly equal size, a number of pieces
+// proportional to the capacity, one workgroup per piece, with a common bound
+// on the piece size chosen so that the pieces fill the grid.  A pruned cache,
+// whose units differ widely in length, thus still spreads evenly over the
+// chip.  Every workgroup derives the same cut from the capacities (wave sums
+// over the units), so no planning launch is needed.  Inside a piece the four waves take
+// 32-row tiles in turn, the next tile's rows in flight while the current one
+// is processed.  The G query heads of a kv head form one 16-column MFMA block
+// (heads >= G are zero), so each K/V row is read once for all of them:
 //   S^T = K Q^T   A = K rows straight from HBM, B = Q (registers)
 //   O^T = V^T P^T A = V^T (per-wave LDS tile, transposing reads), B = P^T
-// Partial (max, sum, O) per split go to the workspace; a second kernel merges
-// them in split order.
+// A unit in one piece is normalised and written directly; the pieces of a
+// split unit leave partial (max, sum, O) results that are merged in row
+// order.
 #include "vc_device.h"
 #include "vc_internal.h"
 
@@ -20,7 +26,7 @@ namespace {
 
 constexpr float kNegInf = -__builtin_inff();
 constexpr float kFloor = -1e30f;
-constexpr int kRowTile = 32;
+constexpr int kRowTile = kDecodeTileRows;
 
 __global__ __launch_bounds__(64) void k_append(int32_t units, int32_t d, uint16_t *k_pool,
                                                uint16_t *v_pool, const int64_t *row_off,
@@ -83,10 +89,9 @@ struct RowTile {
   }
 };
 
-// Partials of the fused step are exchanged between workgroups that may sit
-// on different XCDs (separate L2s): they are written and read with
-// device-coherent accesses instead of fences that would write back and
-// invalidate a whole L2.
+// Partials exchanged inside one launch may cross XCDs (separate L2s): they
+// are written and read with device-coherent accesses instead of fences that
+// would write back and invalidate a whole L2.
 template <bool COHERENT>
 __device__ __forceinline__ void st_part(float *p, float v) {
   if (COHERENT)
@@ -103,32 +108,201 @@ __device__ __forceinline__ float ld_part(const float *p) {
 template <int D>
 struct DecodeSmem {
   static constexpr int PR = D + 16;  // V tile row pitch: conflict-free transposing reads
-  uint16_t vt[4][kRowTile * PR] __attribute__((aligned(16)));
+  static constexpr int kVtBytes = kRowTile * PR * 2;
+  static constexpr int kWoBytes = 16 * (D + 4) * 4;
+  static constexpr int kWaveBytes = kVtBytes > kWoBytes ? kVtBytes : kWoBytes;
+  // Per wave: its V tile while it walks the rows, then its partial O (written
+  // after the wave's last tile, so the two uses never overlap in time).
+  uint8_t wave[4][kWaveBytes] __attribute__((aligned(16)));
   float2 wml[4][16];
-  float wo[4][16][D + 4] __attribute__((aligned(16)));
-  uint32_t last;
+  uint32_t flag[1];
 };
 
-// Attention of the query heads of unit u over cache rows [r0, r1) (row nrow,
-// if >= 0, read from knew / vnew); writes the split's partial (max, sum, O).
-// Where a split's result goes: its partial (plain or device-coherent stores),
-// or, for a unit with a single split, the normalised output itself.
-enum SplitOut { kPartial = 0, kPartialCoherent = 1, kOutput = 2 };
+__device__ __forceinline__ uint16_t *wave_vt(uint8_t *w) { return reinterpret_cast<uint16_t *>(w); }
 
+// Rows of a unit attended by this launch and the index of the row appended
+// by it (-1 if none).  The fused step appends where there is room.
+template <bool STEP>
+__device__ __forceinline__ void unit_rows(int len0, int cap, int max_rows, int &rows, int &nrow) {
+  len0 = max(len0, 0);
+  const bool room = STEP && len0 < cap;
+  rows = room ? len0 + 1 : min(len0, cap);
+  nrow = room ? len0 : -1;
+  rows = max(min(rows, max_rows), 0);
+}
+__device__ __forceinline__ uint32_t unit_tiles(int rows) {
+  return rows > 0 ? (uint32_t)(rows + kRowTile - 1) / kRowTile : 1u;
+}
+
+// Sum over the 64 lanes of a wave, in every lane.
+__device__ __forceinline__ uint32_t wave_sum(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(x), 63);
+}
+
+// ceil(a / b) by a reciprocal, 1 <= b, a + b < 2^32: the rounded product is
+// off by at most one, which the integer check corrects.  With `small`
+// (a + b < 2^20) single precision is close enough; else double.
+struct Recip {
+  uint32_t b;
+  float f;
+  double d;
+};
+__device__ __forceinline__ Recip recip(uint32_t b, bool small) {
+  Recip r;
+  r.b = b;
+  r.f = small ? __builtin_amdgcn_rcpf((float)b) : 0.f;
+  r.d = small ? 0.0 : 1.0 / (double)b;
+  return r;
+}
+__device__ __forceinline__ uint32_t ceil_div(uint32_t a, const Recip &r, bool small) {
+  const uint32_t x = a + r.b - 1;
+  uint32_t q = small ? (uint32_t)((float)x * r.f) : (uint32_t)((double)x * r.d);
+  if ((uint64_t)q * r.b > x) --q;
+  else if ((uint64_t)(q + 1) * r.b <= x) ++q;
+  return q;
+}
+
+// floor(a / b) for a < 2^52, 1 <= b < 2^31 (the reciprocal's error
+// corrected as above; single precision where a < 2^20).
+__device__ __forceinline__ uint64_t floor_div64(uint64_t a, uint32_t b) {
+  const bool small = a < (1u << 20);
+  uint64_t q = small ? (uint64_t)(uint32_t)((float)(uint32_t)a * __builtin_amdgcn_rcpf((float)b))
+                     : (uint64_t)((double)a * (1.0 / (double)b));
+  if (q * b > a) --q;
+  else if ((q + 1) * b <= a) ++q;
+  return q;
+}
+
+// The cut.  The tiles of every unit's capacity (cap rows, at most max_rows)
+// are split into np_u = ceil(tiles_u / c) pieces of nearly equal tile
+// counts, one workgroup each, pieces numbered in unit order.  Capacities do
+// not change during a call, so every workgroup derives the same cut, and a
+// unit's length is read only by its own pieces, the last of which advances it
+// (no grid-wide ordering is needed).  The piece bound c is the smallest of
+// four multiples of 4 tiles (from T / grid up) whose piece count fits the
+// grid, so the four waves of a workgroup get equal numbers of tiles; if none
+// fits, c = T / (grid - U) (rounded up to a multiple of 4) always does, since
+// the pieces then number at most T / c + U.  Each wave computes the whole cut
+// by itself (lane l takes units 64 k + l of each 256-unit chunk), so no
+// barrier is needed; the result, this workgroup's piece, is the same in every
+// wave.
+struct Piece {
+  int32_t u, j, np, p0, nt, len0, cap;  // u = -1: no piece
+  int64_t roff;                         // the unit's first pool row
+};
+
+template <bool STEP>
+__device__ __forceinline__ Piece cut(const DecodePlan &p, uint32_t i) {
+  constexpr int kChunk = 256;  // units per pass: 64 lanes x 4
+  const int lane = threadIdx.x & 63;
+  const int nch = (p.units + kChunk - 1) / kChunk;
+  uint32_t tl[4];
+  int2 lc[4];
+  int64_t ro[4];
+  // 64-unit groups of chunk c that hold units (uniform).
+  auto groups = [&](int c) { return min(4, (p.units - c * kChunk + 63) / 64); };
+  // All loads are issued before any is used (indices clamped rather than
+  // branched on), so they cost one round trip; the row offsets come along so
+  // that the piece's own is at hand without another.
+  auto load = [&](int c) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int uc = min(c * kChunk + k * 64 + lane, p.units - 1);
+      lc[k] = make_int2(ldg(p.len + uc), ldg(p.cap + uc));
+      ro[k] = ldg(p.row_off + uc);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const bool in = c * kChunk + k * 64 + lane < p.units;
+      tl[k] = in ? unit_tiles(max(min(lc[k].y, p.max_rows), 0)) : 0u;
+    }
+  };
+  if (nch == 1) load(0);  // one chunk: its values stay in registers
+  uint32_t T = 0;
+  for (int c = 0; c < nch; ++c) {
+    if (nch > 1) load(c);
+    T += wave_sum(tl[0] + tl[1] + tl[2] + tl[3]);
+  }
+  const uint32_t N = gridDim.x;  // > U (host)
+  const uint32_t c0 = max(4u, (T / N + (T % N != 0) + 3u) & ~3u);
+  const bool small = T + c0 + 16u < (1u << 20);
+  Recip rc[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) rc[q] = recip(c0 + 4u * q, small);
+  uint32_t P[4] = {0u, 0u, 0u, 0u};
+  for (int c = 0; c < nch; ++c) {
+    if (nch > 1) load(c);
+    const int K = groups(c);
+    uint32_t v[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (k >= K) break;  // uniform
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] += tl[k] ? ceil_div(tl[k], rc[q], small) : 0u;
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) P[q] += wave_sum(v[q]);
+  }
+  const uint32_t free_ = N - (uint32_t)p.units;
+  uint32_t cb = ((T / free_ + (T % free_ != 0)) + 3u) & ~3u;
+#pragma unroll
+  for (int q = 3; q >= 0; --q)
+    if (P[q] <= N) cb = c0 + 4u * q;
+  const bool small_b = T + cb < (1u << 20);
+  const Recip rcb = recip(cb, small_b);
+  // Pieces per unit in unit order: lane l's units 64k + l are interleaved,
+  // so the prefix runs over k (outer) and lanes (inner) of each chunk.
+  Piece pc{-1, 0, 0, 0, 0, 0, 0, 0};
+  uint32_t base = 0;
+  for (int c = 0; c < nch; ++c) {
+    if (nch > 1) load(c);
+    const int K = groups(c);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (k >= K) break;  // uniform
+      const uint32_t n = tl[k] ? ceil_div(tl[k], rcb, small_b) : 0u;
+      const uint32_t inc = wave_incl_scan(n);
+      const uint32_t a = base + inc - n;
+      const uint64_t hit = __builtin_amdgcn_ballot_w64(n > 0 && i >= a && i < a + n);
+      if (hit) {
+        const int src = __builtin_ctzll(hit);
+        const int u = c * kChunk + k * 64 + src;
+        pc.u = u;
+        pc.np = __builtin_amdgcn_readlane((int)n, src);
+        pc.p0 = __builtin_amdgcn_readlane((int)a, src);
+        pc.j = (int)i - pc.p0;
+        pc.nt = __builtin_amdgcn_readlane((int)tl[k], src);
+        pc.len0 = __builtin_amdgcn_readlane(lc[k].x, src);
+        pc.cap = __builtin_amdgcn_readlane(lc[k].y, src);
+        const uint32_t rlo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)ro[k], src);
+        const uint32_t rhi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(ro[k] >> 32), src);
+        pc.roff = (int64_t)(((uint64_t)rhi << 32) | rlo);
+      }
+      base += (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
+    }
+  }
+  return pc;
+}
+
+// Where a piece's result goes: its partial (plain or device-coherent stores),
+// or, for a unit attended by one workgroup, the normalised output itself.
+enum PieceOut { kPartial = 0, kPartialCoherent = 1, kOutput = 2 };
+
+// Attention of the query heads of unit u over cache rows [r0, r1) (row nrow,
+// if in range, read from knew / vnew); the result goes to partial slot
+// `slot` or to the output.
 template <int D, int OUT>
-__device__ __forceinline__ void attend_split(const DecodePlan &p, DecodeSmem<D> &sm, int u, int split, int r0,
-                                             int r1, int nrow, const uint16_t *knew, const uint16_t *vnew) {
+__device__ __forceinline__ void attend_piece(const DecodePlan &p, DecodeSmem<D> &sm, int u, int64_t roff, int slot,
+                                             int r0, int r1, int nrow, const uint16_t *knew,
+                                             const uint16_t *vnew) {
   constexpr int KS = D / 32;
   constexpr int MB = D / 16;
   constexpr int PR = DecodeSmem<D>::PR;
-  auto &vt = sm.vt;
   auto &wml = sm.wml;
-  auto &wo = sm.wo;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int g = u % p.Hkv;
   const int lb_ = u / p.Hkv;  // l * B + b
-  const int64_t roff = ldg(p.row_off + u);
   const uint16_t *Kp = p.k_pool + roff * D;
   const uint16_t *Vp = p.v_pool + roff * D;
 
@@ -149,7 +323,7 @@ __device__ __forceinline__ void attend_split(const DecodePlan &p, DecodeSmem<D> 
   // floor so rescaling never forms (-inf) - (-inf).
   float mrow = kFloor, lsum = 0.f;
   const float sc = p.sc;
-  uint16_t *myvt = vt[w];
+  uint16_t *myvt = wave_vt(sm.wave[w]);
   const int tr_row = 4 * lg + (lr >> 2), tr_col = 4 * (lr & 3);
 
   // Wave w takes tiles w, w+4, ...; the next tile's rows are in flight while
@@ -225,16 +399,20 @@ __device__ __forceinline__ void attend_split(const DecodePlan &p, DecodeSmem<D> 
     cur = nxt;
   }
 
-  // Merge the four waves, then store this split's partial.
+  // Merge the four waves, then store this piece's result.  Each wave's O goes
+  // into its own V tile area, which it no longer reads.
   lsum += shfl_xor(lsum, 16);
   lsum += shfl_xor(lsum, 32);
   if (lg == 0) wml[w][lr] = make_float2(mrow <= kFloor ? kNegInf : mrow, lsum);
+  {
+    float(*wo)[D + 4] = reinterpret_cast<float(*)[D + 4]>(sm.wave[w]);
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
+    for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) wo[w][lr][mb * 16 + 4 * lg + i] = O[mb][i];
+      for (int i = 0; i < 4; ++i) wo[lr][mb * 16 + 4 * lg + i] = O[mb][i];
+  }
   __syncthreads();
-  const int64_t pbase = ((int64_t)u * p.nsplit + split) * 16;
+  const int64_t pbase = (int64_t)slot * 16;
   for (int e = tid; e < 16 * D; e += 256) {
     const int h = e / D, x = e % D;
     float M = kNegInf;
@@ -247,13 +425,13 @@ __device__ __forceinline__ void attend_split(const DecodePlan &p, DecodeSmem<D> 
         const float2 ml = wml[i][h];
         if (ml.x != kNegInf) {
           const float f = fast_exp2(ml.x - M);
-          o += f * wo[i][h][x];
+          o += f * reinterpret_cast<const float(*)[D + 4]>(sm.wave[i])[h][x];
           s += f * ml.y;
         }
       }
     }
     if (OUT == kOutput) {
-      // The merge of a single split: its factor is exp2(0) = 1 exactly.
+      // The merge of a single piece: its factor is exp2(0) = 1 exactly.
       if (h < p.G) stg(p.out + ((int64_t)lb_ * p.Hq + (int64_t)g * p.G + h) * D + x, s > 0.f ? o / s : 0.f);
       continue;
     }
@@ -264,115 +442,141 @@ __device__ __forceinline__ void attend_split(const DecodePlan &p, DecodeSmem<D> 
       st_part<OUT == kPartialCoherent>(ml + 1, s);
     }
   }
+  __syncthreads();  // LDS free for the next piece
 }
 
-template <int D>
-__global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
-  __shared__ DecodeSmem<D> sm;
-  const uint32_t lb = xcd_block(blockIdx.x, gridDim.x);
-  const int split = lb % p.nsplit;
-  const int u = lb / p.nsplit;
-  const int len = min(ldg(p.len + u), ldg(p.cap + u));
-  const int r0 = split * p.split_rows;
-  if (r0 >= len && split > 0) return;  // uniform: nothing for this split
-  attend_split<D, kPartial>(p, sm, u, split, r0, min(len, r0 + p.split_rows), -1, nullptr, nullptr);
-}
-
-// Merge the split partials of unit u in split order; out = O / sum (zeros
-// for an empty cache).  Every partial of an output element is loaded in one
-// batch.
+// Merge the np partials of unit u (slots slot0 .. slot0+np-1, in row order);
+// out = O / sum, zeros for an empty cache.  Partials are loaded eight at a
+// time and combined with a running maximum.
 template <int D, bool COHERENT>
-__device__ __forceinline__ void merge_splits(const DecodePlan &p, int u, int ns) {
+__device__ __forceinline__ void merge_pieces(const DecodePlan &p, int u, int slot0, int np) {
+  constexpr int kBatch = 8;
   const int g = u % p.Hkv;
   const int lb_ = u / p.Hkv;
   for (int e = threadIdx.x; e < p.G * D; e += 256) {
     const int h = e / D, x = e % D;
-    float2 ml[kMaxDecodeSplits];
-    float po[kMaxDecodeSplits];
+    float M = kNegInf, o = 0.f, sum = 0.f;
+    for (int j0 = 0; j0 < np; j0 += kBatch) {
+      float2 ml[kBatch];
+      float po[kBatch];
 #pragma unroll
-    for (int s = 0; s < kMaxDecodeSplits; ++s) {
-      const int64_t pb = ((int64_t)u * p.nsplit + s) * 16 + h;
-      const float *mlp = reinterpret_cast<const float *>(p.part_ml + pb);
-      ml[s] = s < ns ? make_float2(ld_part<COHERENT>(mlp), ld_part<COHERENT>(mlp + 1)) : make_float2(kNegInf, 0.f);
-      po[s] = s < ns ? ld_part<COHERENT>(p.part_o + pb * D + x) : 0.f;
-    }
-    float M = kNegInf;
+      for (int k = 0; k < kBatch; ++k) {
+        const bool ok = j0 + k < np;
+        const int64_t pb = (int64_t)(slot0 + j0 + k) * 16 + h;
+        const float *mlp = reinterpret_cast<const float *>(p.part_ml + pb);
+        ml[k] = ok ? make_float2(ld_part<COHERENT>(mlp), ld_part<COHERENT>(mlp + 1)) : make_float2(kNegInf, 0.f);
+        po[k] = ok ? ld_part<COHERENT>(p.part_o + pb * D + x) : 0.f;
+      }
+      float Mc = M;
 #pragma unroll
-    for (int s = 0; s < kMaxDecodeSplits; ++s) M = fmaxf(M, ml[s].x);
-    float o = 0.f, sum = 0.f;
-    if (M != kNegInf) {
+      for (int k = 0; k < kBatch; ++k) Mc = fmaxf(Mc, ml[k].x);
+      if (Mc == kNegInf) continue;
+      if (M != kNegInf && M != Mc) {
+        const float f = fast_exp2(M - Mc);
+        o *= f;
+        sum *= f;
+      }
+      M = Mc;
 #pragma unroll
-      for (int s = 0; s < kMaxDecodeSplits; ++s) {
-        if (ml[s].x == kNegInf) continue;
-        const float f = fast_exp2(ml[s].x - M);
-        o += f * po[s];
-        sum += f * ml[s].y;
+      for (int k = 0; k < kBatch; ++k) {
+        if (ml[k].x == kNegInf) continue;
+        const float f = fast_exp2(ml[k].x - Mc);
+        o += f * po[k];
+        sum += f * ml[k].y;
       }
     }
     stg(p.out + ((int64_t)lb_ * p.Hq + (int64_t)g * p.G + h) * D + x, sum > 0.f ? o / sum : 0.f);
   }
 }
 
-// One decode step in one launch: append (the split holding the new row takes
-// it from k_new / v_new and writes it to the pool), attention per split, and
-// the merge done by the last split of each unit to arrive, which also
-// advances len and re-arms the unit's counter.
-template <int D>
-__global__ __launch_bounds__(256, 2) void k_decode_step(DecodePlan p) {
+// Decode attention over the cut (STEP: the fused step, which also appends
+// the new rows, merges each split unit in the last of its workgroups to
+// finish, and advances the unit's length there).
+template <int D, bool STEP>
+__device__ __forceinline__ void decode_body(const DecodePlan &p) {
   __shared__ DecodeSmem<D> sm;
-  const uint32_t lb = xcd_block(blockIdx.x, gridDim.x);
-  const int split = lb % p.nsplit;
-  const int u = lb / p.nsplit;
-  const int len0 = ldg(p.len + u), cap = ldg(p.cap + u);
-  const bool room = len0 < cap;
-  const int len = room ? len0 + 1 : min(len0, cap);  // rows attended this step
-  // Rows past nsplit * split_rows (a length beyond max_rows) are not attended.
-  const int ns = min(p.nsplit, max(1, (len + p.split_rows - 1) / p.split_rows));
-  // Every launched split of the unit arrives at the counter below, so every
-  // read of len above happens before the last arriver advances it.
-  if (split < ns) {  // uniform
-    const int r0 = split * p.split_rows, r1 = min(len, r0 + p.split_rows);
-    const int nrow = room ? len0 : -1;
-    const uint16_t *knew = p.k_new + (int64_t)u * D, *vnew = p.v_new + (int64_t)u * D;
-    if (room && nrow >= r0 && nrow < r1 && threadIdx.x < 2 * (D / 8)) {
-      const int c = threadIdx.x, cc = c % (D / 8);
-      const int64_t dst = (ldg(p.row_off + u) + nrow) * D + cc * 8;
-      if (c < D / 8)
-        st16(p.k_pool_w + dst, ld16(knew + cc * 8));
-      else
-        st16(p.v_pool_w + dst, ld16(vnew + cc * 8));
+  // Pieces follow the dispatch order, so the workgroups left without a piece
+  // are spread over all XCDs.
+  const uint32_t i = blockIdx.x;
+  const int tid = threadIdx.x;
+  const Piece pc = cut<STEP>(p, i);
+
+  const int u = pc.u, np = pc.np, p0 = pc.p0;
+  if (u >= 0) {
+    int rows, nrow;
+    unit_rows<STEP>(pc.len0, pc.cap, p.max_rows, rows, nrow);
+    // Piece j of np covers tiles [j nt / np, (j + 1) nt / np) of the unit
+    // (nt < 2^26 since rows fit int32, so the products stay below 2^52).
+    const int t0 = (int)floor_div64((uint64_t)pc.j * (uint32_t)pc.nt, (uint32_t)np);
+    const int t1 = (int)floor_div64((uint64_t)(pc.j + 1) * (uint32_t)pc.nt, (uint32_t)np);
+    const int r0 = t0 * kRowTile, r1 = min(rows, t1 * kRowTile);
+    const uint16_t *knew = nullptr, *vnew = nullptr;
+    if (STEP) {
+      knew = p.k_new + (int64_t)u * D;
+      vnew = p.v_new + (int64_t)u * D;
+      // The unit's first piece writes the appended row to the pool; every
+      // piece reads that row from k_new / v_new.
+      if (nrow >= 0 && pc.j == 0 && tid < 2 * (D / 8)) {
+        const int cc = tid % (D / 8);
+        const int64_t dst = (pc.roff + nrow) * D + cc * 8;
+        if (tid < D / 8)
+          st16(p.k_pool_w + dst, ld16(knew + cc * 8));
+        else
+          st16(p.v_pool_w + dst, ld16(vnew + cc * 8));
+      }
+    } else if (pc.j == 0 && tid == 0) {
+      stg(reinterpret_cast<int32_t *>(p.pinfo + u), p0);
+      stg(reinterpret_cast<int32_t *>(p.pinfo + u) + 1, np);
     }
-    if (ns == 1)
-      attend_split<D, kOutput>(p, sm, u, split, r0, r1, nrow, knew, vnew);
+    if (np == 1)
+      attend_piece<D, kOutput>(p, sm, u, pc.roff, 0, r0, r1, nrow, knew, vnew);
     else
-      attend_split<D, kPartialCoherent>(p, sm, u, split, r0, r1, nrow, knew, vnew);
+      attend_piece<D, STEP ? kPartialCoherent : kPartial>(p, sm, u, pc.roff, (int)i, r0, r1, nrow, knew, vnew);
   }
-  if (p.nsplit == 1) {  // the only workgroup of the unit: nothing to merge or count
-    if (threadIdx.x == 0 && room) stg(p.len_w + u, len);
+  if (!STEP || u < 0) return;
+  int rows, nrow;
+  unit_rows<STEP>(pc.len0, pc.cap, p.max_rows, rows, nrow);
+  if (np == 1) {  // the unit's only workgroup: nothing to merge or count
+    if (tid == 0 && nrow >= 0) stg(p.len_w + u, nrow + 1);
     return;
   }
-  // The partial's device-coherent stores complete before the arrival is
-  // counted; the last arriver reads every partial with device-coherent loads.
+  // The partials' device-coherent stores complete before the arrival is
+  // counted; the last arriver reads every partial with device-coherent
+  // loads, merges, advances the length (every piece read it before arriving)
+  // and re-arms the unit's counter.
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  if (threadIdx.x == 0)
-    sm.last = __hip_atomic_fetch_add(p.arrive + u, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-              (uint32_t)(p.nsplit - 1);
+  if (tid == 0)
+    sm.flag[0] = __hip_atomic_fetch_add(p.arrive + u, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                 (uint32_t)(np - 1);
   __syncthreads();
-  if (!sm.last) return;
-  if (ns > 1) merge_splits<D, true>(p, u, ns);
-  if (threadIdx.x == 0) {
+  if (!sm.flag[0]) return;
+  merge_pieces<D, true>(p, u, p0, np);
+  if (tid == 0) {
     __hip_atomic_store(p.arrive + u, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (room) stg(p.len_w + u, len);
+    if (nrow >= 0) stg(p.len_w + u, nrow + 1);
   }
 }
 
-// Merge split partials of each unit (second kernel of the two-call path).
+template <int D>
+__global__ __launch_bounds__(256, 2) void k_decode_attn(DecodePlan p) {
+  decode_body<D, false>(p);
+}
+
+// One decode step in one launch: append, attention and the merge of split
+// units.
+template <int D>
+__global__ __launch_bounds__(256, 2) void k_decode_step(DecodePlan p) {
+  decode_body<D, true>(p);
+}
+
+// Merge the pieces of each split unit (second kernel of the two-call path).
 template <int D>
 __global__ __launch_bounds__(256) void k_decode_combine(DecodePlan p) {
   const int u = blockIdx.x;
-  const int len = min(ldg(p.len + u), ldg(p.cap + u));
-  merge_splits<D, false>(p, u, len > 0 ? min(p.nsplit, (len + p.split_rows - 1) / p.split_rows) : 1);
+  const int slot0 = ldg(reinterpret_cast<const int32_t *>(p.pinfo + u));
+  const int np = ldg(reinterpret_cast<const int32_t *>(p.pinfo + u) + 1);
+  if (np > 1) merge_pieces<D, false>(p, u, slot0, np);
 }
 
 }  // namespace
@@ -387,26 +591,22 @@ hipError_t launch_append(int32_t units, int32_t d, uint16_t *k_pool, uint16_t *v
 }
 
 hipError_t launch_decode_step(const DecodePlan &p, hipStream_t st) {
-  const int units = p.L * p.B * p.Hkv;
-  if (units == 0) return hipSuccess;
-  const uint32_t grid = (uint32_t)units * p.nsplit;
+  if (p.units == 0 || p.nwg < 1) return hipSuccess;
   if (p.d == 128)
-    hipLaunchKernelGGL(k_decode_step<128>, dim3(grid), dim3(256), 0, st, p);
+    hipLaunchKernelGGL(k_decode_step<128>, dim3(p.nwg), dim3(256), 0, st, p);
   else
-    hipLaunchKernelGGL(k_decode_step<64>, dim3(grid), dim3(256), 0, st, p);
+    hipLaunchKernelGGL(k_decode_step<64>, dim3(p.nwg), dim3(256), 0, st, p);
   return hipGetLastError();
 }
 
 hipError_t launch_decode(const DecodePlan &p, hipStream_t st) {
-  const int units = p.L * p.B * p.Hkv;
-  if (units == 0) return hipSuccess;
-  const uint32_t grid = (uint32_t)units * p.nsplit;
+  if (p.units == 0 || p.nwg < 1) return hipSuccess;
   if (p.d == 128) {
-    hipLaunchKernelGGL(k_decode_attn<128>, dim3(grid), dim3(256), 0, st, p);
-    hipLaunchKernelGGL(k_decode_combine<128>, dim3(units), dim3(256), 0, st, p);
+    hipLaunchKernelGGL(k_decode_attn<128>, dim3(p.nwg), dim3(256), 0, st, p);
+    hipLaunchKernelGGL(k_decode_combine<128>, dim3(p.units), dim3(256), 0, st, p);
   } else {
-    hipLaunchKernelGGL(k_decode_attn<64>, dim3(grid), dim3(256), 0, st, p);
-    hipLaunchKernelGGL(k_decode_combine<64>, dim3(units), dim3(256), 0, st, p);
+    hipLaunchKernelGGL(k_decode_attn<64>, dim3(p.nwg), dim3(256), 0, st, p);
+    hipLaunchKernelGGL(k_decode_combine<64>, dim3(p.units), dim3(256), 0, st, p);
   }
   return hipGetLastError();
 }

@@ -383,36 +383,71 @@ vc_status check_decode(const vc_decode_shape *s) {
   if (!s) return VC_ERR_ARG;
   if (s->B < 1 || s->L < 1 || s->Hq < 1 || s->Hkv < 1) return VC_ERR_SHAPE;
   if (s->Hq % s->Hkv != 0) return VC_ERR_SHAPE;
+  if ((int64_t)s->L * s->B * s->Hq > INT32_MAX) return VC_ERR_SHAPE;
   if (s->Hq / s->Hkv > 16) return VC_ERR_UNSUPPORTED;
   if (s->d != 64 && s->d != 128) return VC_ERR_UNSUPPORTED;
   return VC_OK;
 }
 
-// Row splits of decode attention: enough splits per unit that the grid fills
-// about one round of resident workgroups (512), each split at least 256 rows
-// (short caches stay in one split and skip the merge), at most
-// kMaxDecodeSplits splits of at most kDecodeSplitRows rows.
-struct DecodeSplit {
-  int32_t n, rows;
+// Workspace layout of the decode calls: partial O and (max, sum) per piece
+// (workgroup), then the (first piece, pieces) table of the units; the fused
+// step adds one arrival counter per unit.
+struct DecodeWs {
+  size_t o, ml, pinfo, arrive, base, step;
 };
-DecodeSplit decode_split(const vc_decode_shape *s, int64_t max_rows) {
-  const int64_t units = std::max<int64_t>(1, (int64_t)s->L * s->B * s->Hkv);
-  const int64_t want = std::min<int64_t>(kMaxDecodeSplits, std::max<int64_t>(1, 512 / units));
-  int64_t rows = (std::max<int64_t>(1, max_rows) + want - 1) / want;
-  rows = std::max<int64_t>(256, (rows + 31) & ~int64_t(31));
-  rows = std::min<int64_t>(rows, kDecodeSplitRows);
-  const int64_t n = std::max<int64_t>(1, (max_rows + rows - 1) / rows);
-  return {(int32_t)n, (int32_t)rows};
+DecodeWs decode_ws(int64_t units, int64_t nwg, int d) {
+  const size_t slots = (size_t)nwg;
+  DecodeWs w{};
+  w.o = 0;
+  w.ml = align_up(sizeof(float) * slots * 16 * (size_t)d);
+  w.pinfo = w.ml + align_up(sizeof(float2) * slots * 16);
+  w.arrive = w.pinfo + align_up(sizeof(int2) * (size_t)units);
+  w.base = w.arrive;
+  w.step = w.arrive + align_up(sizeof(uint32_t) * (size_t)units);
+  return w;
+}
+
+// Plan of a decode call, or a status if it cannot run.
+vc_status decode_plan(const vc_decode_shape *s, const vc_cache *c, const void *q, float *out, float scale,
+                      int64_t max_rows, DecodePlan &p) {
+  vc_status st = check_decode(s);
+  if (st != VC_OK) return st;
+  if (!c || !c->k_pool || !c->v_pool || !c->row_off || !c->cap || !c->len || !q || !out) return VC_ERR_ARG;
+  if (!(scale > 0.f) || !std::isfinite(scale) || max_rows < 0) return VC_ERR_ARG;
+  const int64_t units = (int64_t)s->L * s->B * s->Hkv;
+  const int32_t nwg = decode_grid(units, max_rows);
+  if (nwg < 1) return VC_ERR_UNSUPPORTED;
+  p = DecodePlan{};
+  p.B = s->B; p.L = s->L; p.Hq = s->Hq; p.Hkv = s->Hkv; p.d = s->d; p.G = s->Hq / s->Hkv;
+  p.units = (int32_t)units;
+  p.max_rows = (int32_t)std::min<int64_t>(max_rows, INT32_MAX);
+  p.nwg = nwg;
+  p.sc = scale * 1.4426950408889634f;
+  p.k_pool = static_cast<const uint16_t *>(c->k_pool);
+  p.v_pool = static_cast<const uint16_t *>(c->v_pool);
+  p.row_off = c->row_off;
+  p.cap = c->cap;
+  p.len = c->len;
+  p.q = static_cast<const uint16_t *>(q);
+  p.out = out;
+  return VC_OK;
+}
+
+void decode_bind_ws(DecodePlan &p, uint8_t *ws) {
+  const DecodeWs w = decode_ws(p.units, p.nwg, p.d);
+  p.part_o = reinterpret_cast<float *>(ws + w.o);
+  p.part_ml = reinterpret_cast<float2 *>(ws + w.ml);
+  p.pinfo = reinterpret_cast<int2 *>(ws + w.pinfo);
+  p.arrive = reinterpret_cast<uint32_t *>(ws + w.arrive);
 }
 }  // namespace
 
 size_t viscache_decode_workspace_bytes(const vc_decode_shape *s, int64_t max_rows) {
   if (check_decode(s) != VC_OK || max_rows < 0) return 0;
-  if (max_rows > (int64_t)kDecodeSplitRows * kMaxDecodeSplits) return 0;
   const int64_t units = (int64_t)s->L * s->B * s->Hkv;
-  const int64_t ns = decode_split(s, max_rows).n;
-  return align_up(sizeof(float) * (size_t)(units * ns * 16 * s->d)) +
-         align_up(sizeof(float2) * (size_t)(units * ns * 16));
+  const int32_t nwg = decode_grid(units, max_rows);
+  if (nwg < 1) return 0;
+  return decode_ws(units, nwg, s->d).base;
 }
 
 vc_status viscache_append_kv(const vc_decode_shape *s, const vc_cache *c, const void *k_new,
@@ -432,78 +467,42 @@ vc_status viscache_append_kv(const vc_decode_shape *s, const vc_cache *c, const 
 vc_status viscache_decode_attn(const vc_decode_shape *s, const vc_cache *c, const void *q, float *out,
                                float scale, int64_t max_rows, void *workspace, size_t workspace_bytes,
                                void *stream) {
-  vc_status st = check_decode(s);
+  DecodePlan p;
+  const vc_status st = decode_plan(s, c, q, out, scale, max_rows, p);
   if (st != VC_OK) return st;
-  if (!c || !c->k_pool || !c->v_pool || !c->row_off || !c->cap || !c->len || !q || !out) return VC_ERR_ARG;
-  if (!(scale > 0.f) || !std::isfinite(scale) || max_rows < 0) return VC_ERR_ARG;
-  if (max_rows > (int64_t)kDecodeSplitRows * kMaxDecodeSplits) return VC_ERR_UNSUPPORTED;
   const size_t need = viscache_decode_workspace_bytes(s, max_rows);
   if (!workspace || workspace_bytes < need) return VC_ERR_WORKSPACE;
   if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return VC_ERR_WORKSPACE;
-  const int64_t units = (int64_t)s->L * s->B * s->Hkv;
-  DecodePlan p{};
-  p.B = s->B; p.L = s->L; p.Hq = s->Hq; p.Hkv = s->Hkv; p.d = s->d; p.G = s->Hq / s->Hkv;
-  const DecodeSplit sp = decode_split(s, max_rows);
-  p.nsplit = sp.n;
-  p.split_rows = sp.rows;
-  p.sc = scale * 1.4426950408889634f;
-  p.k_pool = static_cast<const uint16_t *>(c->k_pool);
-  p.v_pool = static_cast<const uint16_t *>(c->v_pool);
-  p.row_off = c->row_off;
-  p.cap = c->cap;
-  p.len = c->len;
-  p.q = static_cast<const uint16_t *>(q);
-  p.out = out;
-  uint8_t *ws = static_cast<uint8_t *>(workspace);
-  p.part_o = reinterpret_cast<float *>(ws);
-  p.part_ml = reinterpret_cast<float2 *>(ws + align_up(sizeof(float) * (size_t)(units * p.nsplit * 16 * s->d)));
+  decode_bind_ws(p, static_cast<uint8_t *>(workspace));
+  p.arrive = nullptr;
   if (launch_decode(p, static_cast<hipStream_t>(stream)) != hipSuccess) return VC_ERR_HIP;
   return VC_OK;
 }
 
 size_t viscache_decode_step_workspace_bytes(const vc_decode_shape *s, int64_t max_rows) {
-  const size_t base = viscache_decode_workspace_bytes(s, max_rows);
-  if (base == 0) return 0;
+  if (check_decode(s) != VC_OK || max_rows < 0) return 0;
   const int64_t units = (int64_t)s->L * s->B * s->Hkv;
-  return base + align_up(sizeof(uint32_t) * (size_t)units);
+  const int32_t nwg = decode_grid(units, max_rows);
+  if (nwg < 1) return 0;
+  return decode_ws(units, nwg, s->d).step;
 }
 
 vc_status viscache_decode_step(const vc_decode_shape *s, const vc_cache *c, const void *k_new,
                                const void *v_new, const void *q, float *out, float scale, int64_t max_rows,
                                void *workspace, size_t workspace_bytes, void *stream) {
-  vc_status st = check_decode(s);
+  DecodePlan p;
+  const vc_status st = decode_plan(s, c, q, out, scale, max_rows, p);
   if (st != VC_OK) return st;
-  if (!c || !c->k_pool || !c->v_pool || !c->row_off || !c->cap || !c->len || !q || !out || !k_new || !v_new)
-    return VC_ERR_ARG;
-  if (!(scale > 0.f) || !std::isfinite(scale) || max_rows < 0) return VC_ERR_ARG;
-  if (max_rows > (int64_t)kDecodeSplitRows * kMaxDecodeSplits) return VC_ERR_UNSUPPORTED;
-  const size_t base = viscache_decode_workspace_bytes(s, max_rows);
+  if (!k_new || !v_new) return VC_ERR_ARG;
   const size_t need = viscache_decode_step_workspace_bytes(s, max_rows);
   if (!workspace || workspace_bytes < need) return VC_ERR_WORKSPACE;
   if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return VC_ERR_WORKSPACE;
-  const int64_t units = (int64_t)s->L * s->B * s->Hkv;
-  DecodePlan p{};
-  p.B = s->B; p.L = s->L; p.Hq = s->Hq; p.Hkv = s->Hkv; p.d = s->d; p.G = s->Hq / s->Hkv;
-  const DecodeSplit sp = decode_split(s, max_rows);
-  p.nsplit = sp.n;
-  p.split_rows = sp.rows;
-  p.sc = scale * 1.4426950408889634f;
-  p.k_pool = static_cast<const uint16_t *>(c->k_pool);
-  p.v_pool = static_cast<const uint16_t *>(c->v_pool);
+  decode_bind_ws(p, static_cast<uint8_t *>(workspace));
   p.k_pool_w = static_cast<uint16_t *>(c->k_pool);
   p.v_pool_w = static_cast<uint16_t *>(c->v_pool);
-  p.row_off = c->row_off;
-  p.cap = c->cap;
-  p.len = c->len;
   p.len_w = c->len;
-  p.q = static_cast<const uint16_t *>(q);
-  p.out = out;
   p.k_new = static_cast<const uint16_t *>(k_new);
   p.v_new = static_cast<const uint16_t *>(v_new);
-  uint8_t *ws = static_cast<uint8_t *>(workspace);
-  p.part_o = reinterpret_cast<float *>(ws);
-  p.part_ml = reinterpret_cast<float2 *>(ws + align_up(sizeof(float) * (size_t)(units * p.nsplit * 16 * s->d)));
-  p.arrive = reinterpret_cast<uint32_t *>(ws + base);
   if (launch_decode_step(p, static_cast<hipStream_t>(stream)) != hipSuccess) return VC_ERR_HIP;
   return VC_OK;
 }

@@ -78,13 +78,34 @@ hipError_t launch_score_global(const PrunePlan &p, hipStream_t st);
 hipError_t launch_select(const PrunePlan &p, hipStream_t st);
 hipError_t launch_fuse(const PrunePlan &p, hipStream_t st);
 
-constexpr int kDecodeSplitRows = 1024;  // most cache rows per decode workgroup
-constexpr int kMaxDecodeSplits = 32;    // => at most 32768 cached rows per unit
+// Decode work is dealt out in 32-row tiles: the tiles of each unit's capacity
+// are split into pieces, one workgroup per piece (the device picks the piece
+// size).
+constexpr int kDecodeTileRows = 32;
+constexpr int kDecodeSlots = 512;  // resident decode workgroups (256 CUs x 2)
+
+// Workgroups of a decode launch over `units` caches of at most max_rows rows:
+// the resident slots (more for many units: each unit takes at least one
+// piece), at most the pieces of 4 tiles the rows can form, and always more
+// than `units`, which the device's fallback piece size relies on.  0 if the
+// tile count of the bound does not fit 31 bits.
+inline int32_t decode_grid(int64_t units, int64_t max_rows) {
+  if (units < 1 || max_rows < 0 || max_rows > (int64_t(1) << 40)) return 0;
+  const int64_t per = max_rows == 0 ? 1 : (max_rows + kDecodeTileRows - 1) / kDecodeTileRows;
+  if (per > ((int64_t(1) << 31) - 1) / units) return 0;
+  int64_t n = units + kDecodeSlots / 2;
+  if (n < kDecodeSlots) n = kDecodeSlots;
+  const int64_t most = units * ((per + 3) / 4);
+  if (n > most) n = most;
+  if (n < units + 1) n = units + 1;
+  return n > INT32_MAX ? 0 : (int32_t)n;
+}
 
 struct DecodePlan {
   int32_t B, L, Hq, Hkv, d, G;
-  int32_t nsplit;    // row splits per unit
-  int32_t split_rows;
+  int32_t units;     // L * B * Hkv
+  int32_t max_rows;  // rows past this index are not attended
+  int32_t nwg;       // workgroups of the launch (decode_grid)
   float sc;          // scale * log2(e)
   const uint16_t *k_pool, *v_pool;
   const int64_t *row_off;
@@ -92,12 +113,16 @@ struct DecodePlan {
   const int32_t *len;
   const uint16_t *q;
   float *out;
-  float *part_o;     // [U][nsplit][16][d]
-  float2 *part_ml;   // [U][nsplit][16]
+  // Partial results of split units, one slot per piece (workgroup):
+  // [nwg][16][d] and [nwg][16] (max, sum).
+  float *part_o;
+  float2 *part_ml;
+  int2 *pinfo;       // [U] (first slot, pieces) of each unit (two-call path)
   // Fused step only: the row to append per unit ([U][d] each), the arrival
-  // counters of the split merge, and the writable views of pools and lengths.
+  // counters of the split units ([U], zero between calls) and the writable
+  // views of pools and lengths.
   const uint16_t *k_new, *v_new;
-  uint32_t *arrive;  // [U], zero between calls
+  uint32_t *arrive;
   uint16_t *k_pool_w, *v_pool_w;
   int32_t *len_w;
 };

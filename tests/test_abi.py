@@ -150,12 +150,17 @@ def test_decode_rejects_bad_arguments(vc):
 
 
 def test_decode_row_limit(vc):
-    """Caches longer than 32 splits of 1024 rows are refused on the host."""
+    """Long caches are accepted: the workspace holds one partial per
+    workgroup, and the grid stops growing once it fills the resident slots,
+    so it does not grow with the rows; a row bound whose tile count overflows
+    31 bits is refused on the host."""
     ds = vc.vc_decode_shape(1, 2, 8, 2, 128)
-    assert vc.viscache_decode_workspace_bytes(ds, 32768) > 0
-    assert vc.viscache_decode_workspace_bytes(ds, 32769) == 0
+    big = vc.viscache_decode_workspace_bytes(ds, 1 << 28)
+    assert big == vc.viscache_decode_workspace_bytes(ds, 32768) > vc.viscache_decode_workspace_bytes(ds, 64) > 0
+    assert vc.viscache_decode_step_workspace_bytes(ds, 1 << 28) > big
+    assert vc.viscache_decode_workspace_bytes(ds, 1 << 35) == 0
+    assert vc.viscache_decode_step_workspace_bytes(ds, 1 << 35) == 0
     c = vc.vc_cache(256, 256, 256, 256, 256)
-    need = vc.viscache_decode_workspace_bytes(ds, 32768)
     with pytest.raises(vc.VisCacheError) as ei:
-        vc.viscache_decode_attn(ds, c, 256, 256, 0.1, 32769, 256, need, 0)
+        vc.viscache_decode_attn(ds, c, 256, 256, 0.1, 1 << 35, 256, big, 0)
     assert ei.value.status == vc.VC_ERR_UNSUPPORTED

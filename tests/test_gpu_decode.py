@@ -37,8 +37,8 @@ def test_decode_random_caches(dev, orc, sg, d, Hq, Hkv):
     from synthgen.device import bf16_tensor, to_host_bf16
     L, B = 2, 2
     units = L * B * Hkv
-    # Empty, sub-tile, tile edges, split edges (1024 rows per split) and
-    # several splits.
+    # Empty, sub-tile and tile edges, and units long enough to be cut over
+    # several workgroups.
     lens = [0, 1, 31, 33, 3100, 511, 1023, 1024, 1100, 5, 64, 2049, 2, 1025, 47, 4097][:units]
     lens += [17] * (units - len(lens))
     caps = [x + 3 for x in lens]
@@ -157,7 +157,8 @@ def test_decode_step_matches_append_then_attend(dev, orc, sg, d, Hq, Hkv):
     """viscache_decode_step (one launch) against viscache_append_kv followed by
     viscache_decode_attn on a copy of the same cache, over several steps:
     identical outputs (bit for bit), lengths and pools; the oracle checks the
-    attention.  Lengths cross tile and split edges and reach capacity."""
+    attention.  Lengths cross tile edges, units are cut over several
+    workgroups, and one reaches capacity."""
     from paper_2608_24063_amd.tensors import DecodeCache
     from synthgen.device import bf16_tensor, to_host_bf16
     L, B = 2, 1
@@ -205,7 +206,67 @@ def test_decode_step_matches_append_then_attend(dev, orc, sg, d, Hq, Hkv):
                     h = g * G + hh
                     _check_out(orc, q[l, b, h], K[r0:r0 + n], V[r0:r0 + n], o[l, b, h], scale,
                                f"step l={l} g={g} h={h} n={n}")
-    # The arrival counters (after the decode partials) are back at zero.
+    _counters_zero(c, units)
+
+
+def _counters_zero(c, units):
+    """The fused step's arrival counters (after the decode workspace) are
+    back at zero."""
     import paper_2608_24063_amd as vc
     base = vc.viscache_decode_workspace_bytes(c.shape, c.max_cap)
     assert int(c.step_ws[base:base + 4 * units].view(torch.int32).abs().sum()) == 0
+
+
+def test_decode_many_units_and_long_unit(dev, orc, sg):
+    """More units than one pass of the block prefix sum covers (1280), most
+    of them short or empty, and one 40000-row unit cut into more than a
+    hundred pieces (a grid beyond the resident slots, merges of many
+    partials): the fused step equals append + attend bit for bit, and the
+    oracle checks every unit."""
+    from paper_2608_24063_amd.tensors import DecodeCache
+    from synthgen.device import bf16_tensor, to_host_bf16
+    L, B, Hq, Hkv, d = 2, 80, 16, 8, 64
+    units = L * B * Hkv
+    rng = np.random.default_rng(5)
+    lens = [int(x) for x in rng.integers(0, 70, size=units)]
+    lens[3], lens[700], lens[1279] = 40000, 5000, 0
+    caps = [x + 2 for x in lens]
+    caps[1279] = 0  # no room at all
+    a = DecodeCache(L, B, Hq, Hkv, d, caps, dev)
+    c = DecodeCache(L, B, Hq, Hkv, d, caps, dev)
+    Kp = _bits(sg, 31, 1, (a.total_rows, d))
+    Vp = _bits(sg, 31, 2, (a.total_rows, d))
+    for cc in (a, c):
+        cc.k_pool.copy_(bf16_tensor(Kp, dev))
+        cc.v_pool.copy_(bf16_tensor(Vp, dev))
+        cc.len.copy_(torch.tensor(lens, dtype=torch.int32))
+    scale = d ** -0.5
+    kn = _bits(sg, 32, 1, (L, B, Hkv, d))
+    vn = _bits(sg, 32, 2, (L, B, Hkv, d))
+    q = _bits(sg, 32, 3, (L, B, Hq, d))
+    kt, vt, qt = bf16_tensor(kn, dev), bf16_tensor(vn, dev), bf16_tensor(q, dev)
+    out_a = torch.full((L, B, Hq, d), float("nan"), dtype=torch.float32, device=dev)
+    out_c = torch.full((L, B, Hq, d), float("nan"), dtype=torch.float32, device=dev)
+    a.append(kt, vt)
+    a.attend(qt, out_a, scale)
+    c.step(kt, vt, qt, out_c, scale)
+    torch.cuda.synchronize()
+    assert torch.equal(out_a, out_c), "fused step differs from append + attend"
+    cur = [min(x + 1, cap) for x, cap in zip(lens, caps)]
+    assert c.len.cpu().tolist() == cur and a.len.cpu().tolist() == cur
+    assert torch.equal(a.k_pool, c.k_pool) and torch.equal(a.v_pool, c.v_pool)
+    _counters_zero(c, units)
+    K = to_host_bf16(c.k_pool)
+    V = to_host_bf16(c.v_pool)
+    o = out_c.cpu().numpy()
+    G = Hq // Hkv
+    for l in range(L):
+        for b in range(B):
+            for g in range(Hkv):
+                u = (l * B + b) * Hkv + g
+                r0, n = c.offs_host[u], cur[u]
+                h = g * G + (u % G)
+                if n == 0:
+                    assert np.all(o[l, b, g * G:(g + 1) * G] == 0)
+                    continue
+                _check_out(orc, q[l, b, h], K[r0:r0 + n], V[r0:r0 + n], o[l, b, h], scale, f"u={u} n={n}")
