@@ -166,26 +166,51 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p) {
   const float *Q = reinterpret_cast<const float *>(ldg(p.lp + LP_Q * p.L + ls)) + qoff;
   uint16_t *Qb = p.qbf + (int64_t)ls * p.B * p.Hq * p.W * D + qoff;
 
-  // Query rows -> bf16 B operands (round to nearest even), zero past R.
+  // Query rows -> bf16 B operands (round to nearest even), zero past R.  All
+  // loads of a half (two 16-row blocks) are issued before any is used (rows
+  // clamped rather than branched on), so the prologue costs two round trips
+  // instead of one per load pair.
   const int row0 = qg * kStatsRows + w * 64;
   const bool active = row0 < p.R;  // wave-uniform: waves of padding rows only stage tiles
   bf16x8 bq[4][KS];
 #pragma unroll
-  for (int qb = 0; qb < 4; ++qb) {
-    const int row = row0 + qb * 16 + lr;
+  for (int hq = 0; hq < 2; ++hq) {
+    u32x4 raw[2][KS][2];
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      u32x4 pk = {0, 0, 0, 0};
-      if (row < p.R) {
-        const float *src = Q + (int64_t)row * D + 32 * s + 8 * lg;
-        const u32x4 a = ld16(src), c = ld16(src + 4);
-        pk = u32x4{pack_bf16(__uint_as_float(a.x), __uint_as_float(a.y)),
-                   pack_bf16(__uint_as_float(a.z), __uint_as_float(a.w)),
-                   pack_bf16(__uint_as_float(c.x), __uint_as_float(c.y)),
-                   pack_bf16(__uint_as_float(c.z), __uint_as_float(c.w))};
-        if (ks == 0) st16(Qb + (int64_t)row * D + 32 * s + 8 * lg, pk);
+    for (int qq = 0; qq < 2; ++qq) {
+      const int rc = min(row0 + (2 * hq + qq) * 16 + lr, p.R - 1);
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const float *src = Q + (int64_t)rc * D + 32 * s + 8 * lg;
+        raw[qq][s][0] = ld16(src);
+        raw[qq][s][1] = ld16(src + 4);
       }
-      bq[qb][s] = as_bf16x8(pk);
+    }
+#pragma unroll
+    for (int qq = 0; qq < 2; ++qq) {
+      const int qb = 2 * hq + qq;
+      const int row = row0 + qb * 16 + lr;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const u32x4 a = raw[qq][s][0], c = raw[qq][s][1];
+        u32x4 pk = {pack_bf16(__uint_as_float(a.x), __uint_as_float(a.y)),
+                    pack_bf16(__uint_as_float(a.z), __uint_as_float(a.w)),
+                    pack_bf16(__uint_as_float(c.x), __uint_as_float(c.y)),
+                    pack_bf16(__uint_as_float(c.z), __uint_as_float(c.w))};
+        if (row >= p.R) pk = u32x4{0, 0, 0, 0};
+        bq[qb][s] = as_bf16x8(pk);
+      }
+    }
+  }
+  // The first key split also leaves the bf16 queries for the column pass.
+  if (ks == 0) {
+#pragma unroll
+    for (int qb = 0; qb < 4; ++qb) {
+      const int row = row0 + qb * 16 + lr;
+      if (row < p.R) {
+#pragma unroll
+        for (int s = 0; s < KS; ++s) st16(Qb + (int64_t)row * D + 32 * s + 8 * lg, as_u32x4(bq[qb][s]));
+      }
     }
   }
 
