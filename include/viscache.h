@@ -71,7 +71,10 @@ typedef struct {
 
 /* Problem shape.  L layers, Hq query heads, Hkv kv heads (Hq % Hkv == 0;
  * query head hq reads kv head hq / (Hq/Hkv)), head dim d in {64, 128},
- * W window queries per head, B sequences with n_vis[b] visual tokens each. */
+ * W window queries per head, B sequences with n_vis[b] visual tokens each.
+ * VC_ERR_UNSUPPORTED beyond the kernels' limits: d, (Hq/Hkv)*W > 1024,
+ * n_vis[b] > 32768, or 56*L + 12*B + 16 > 30720 (the layer table and the
+ * per-sequence offsets must fit the first 30 KB of the launch plan). */
 typedef struct {
   int32_t B, L, Hq, Hkv, d, W;
   const int32_t *n_vis; /* HOST array [B]; each entry in [0, 32768] */
@@ -154,10 +157,11 @@ vc_status viscache_prune(const vc_shape *shape, const vc_params *params, const v
 /* Device, asynchronous.  viscache_prune with stage timing: `events` is a HOST
  * array of VC_PRUNE_EVENTS hipEvent_t handles (passed as void*) created by the
  * caller; event i is recorded on `stream` before stage i and the last one
- * after the final stage.  Stages: 0 plan upload, 1 score row statistics,
- * 2 score column sums, 3 shared-score reduction (empty in LAYER_HEAD mode),
- * 4 keep/drop selection, 5 key gather and value fusion.  events == NULL
- * behaves exactly as viscache_prune. */
+ * after the final stage.  Stages: 0 plan upload past its first 30 KB
+ * (empty for most shapes: the first 30 KB travel with stage 1), 1 score row
+ * statistics, 2 score column sums, 3 shared-score reduction (empty in
+ * LAYER_HEAD mode), 4 keep/drop selection, 5 key gather and value fusion.
+ * events == NULL behaves exactly as viscache_prune. */
 vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params,
                                 const vc_prune_io *io, void *workspace, size_t workspace_bytes,
                                 void *stream, void *const *events);

@@ -137,11 +137,22 @@ __device__ __forceinline__ void stats_tile(const uint16_t *kl, const bf16x8 (&bq
   }
 }
 
-template <int D>
-__global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p) {
+// A 64-bit table entry of the plan chunk (two words, low first).
+template <uint32_t CW>
+__device__ __forceinline__ uint64_t chunk_u64(const UploadChunk<CW> &c, int w) {
+  return (uint64_t)c.data[w] | ((uint64_t)c.data[w + 1] << 32);
+}
+
+// The plan's first chunk arrives with this launch: the grid copies it into
+// the workspace for the later kernels, and every workgroup reads its own
+// tables (layer pointers, token offsets, lengths) from the argument itself.
+template <int D, uint32_t CW>
+__global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p, uint32_t *plan_dst, UploadChunk<CW> c) {
   constexpr int KS = D / 32;
   constexpr int P = kPitch<D>;
   __shared__ __attribute__((aligned(16))) uint16_t kt[2][kKeyTile * P];
+
+  for (uint32_t i = blockIdx.x * 256 + threadIdx.x; i < c.words; i += gridDim.x * 256) plan_dst[i] = c.data[i];
 
   const uint32_t lb = xcd_block(blockIdx.x, gridDim.x);
   const int qg = lb % p.nqg;
@@ -149,8 +160,8 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p) {
   const int u = lb / (p.nqg * p.nks);
   int ls, b, g;
   unit_coords(p, u, ls, b, g);
-  const int n = ldg(p.nb + b);
-  const int64_t toff = ldg(p.toff + b);
+  const int n = (int)c.data[p.w_nb + b];
+  const int64_t toff = (int64_t)chunk_u64(c, p.w_toff + 2 * b);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const float sc = p.sc;
@@ -160,10 +171,10 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p) {
   const int span = ((n + p.nks - 1) / p.nks + kKeyTile - 1) & ~(kKeyTile - 1);
   const int k0 = min(n, ks * span), k1 = min(n, k0 + span);
 
-  const uint16_t *K = reinterpret_cast<const uint16_t *>(ldg(p.lp + LP_K_IN * p.L + ls)) +
+  const uint16_t *K = reinterpret_cast<const uint16_t *>(chunk_u64(c, p.w_lp + 2 * (LP_K_IN * p.L + ls))) +
                       (toff * p.Hkv + (int64_t)g * n) * D;
   const int64_t qoff = ((int64_t)b * p.Hq + (int64_t)g * p.G) * p.W * D;
-  const float *Q = reinterpret_cast<const float *>(ldg(p.lp + LP_Q * p.L + ls)) + qoff;
+  const float *Q = reinterpret_cast<const float *>(chunk_u64(c, p.w_lp + 2 * (LP_Q * p.L + ls))) + qoff;
   uint16_t *Qb = p.qbf + (int64_t)ls * p.B * p.Hq * p.W * D + qoff;
 
   // Query rows -> bf16 B operands (round to nearest even), zero past R.  All
@@ -402,15 +413,30 @@ __global__ __launch_bounds__(256) void k_score_global(PrunePlan p) {
 
 }  // namespace
 
-hipError_t launch_score_stats(const PrunePlan &p, hipStream_t st) {
+namespace {
+template <uint32_t CW>
+hipError_t stats_with_chunk(const PrunePlan &p, uint32_t grid, uint32_t *dst, const uint8_t *src, uint32_t words,
+                            hipStream_t st) {
+  UploadChunk<CW> c;
+  c.words = words;
+  c.pad = 0;
+  __builtin_memcpy(c.data, src, (size_t)words * 4);
+  if (p.d == 128)
+    hipLaunchKernelGGL((k_score_stats<128, CW>), dim3(grid), dim3(256), 0, st, p, dst, c);
+  else
+    hipLaunchKernelGGL((k_score_stats<64, CW>), dim3(grid), dim3(256), 0, st, p, dst, c);
+  return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_score_stats(const PrunePlan &p, uint32_t *dst, const uint8_t *src, uint32_t words,
+                              hipStream_t st) {
   const int units = p.Ls * p.B * p.Hkv;
   const uint32_t grid = (uint32_t)units * p.nqg * p.nks;
-  if (grid == 0) return hipSuccess;
-  if (p.d == 128)
-    hipLaunchKernelGGL(k_score_stats<128>, dim3(grid), dim3(256), 0, st, p);
-  else
-    hipLaunchKernelGGL(k_score_stats<64>, dim3(grid), dim3(256), 0, st, p);
-  return hipGetLastError();
+  if (grid == 0 || words > kChunkWords) return hipErrorInvalidValue;
+  return words <= kChunkWordsSmall ? stats_with_chunk<kChunkWordsSmall>(p, grid, dst, src, words, st)
+         : words <= kChunkWordsMid ? stats_with_chunk<kChunkWordsMid>(p, grid, dst, src, words, st)
+                                   : stats_with_chunk<kChunkWords>(p, grid, dst, src, words, st);
 }
 
 hipError_t launch_score_colsum(const PrunePlan &p, hipStream_t st) {

@@ -1,25 +1,15 @@
 // k_setup.hip -- moves the host-built prune plan (layer pointer table, budgets,
 // offsets, fusion unit records) into the device workspace.  The plan travels
-// as kernel arguments, up to 30 KB per launch (one launch for the shapes seen
-// in practice), so no host buffer has to outlive the call and nothing is
-// copied through pageable memory.
+// as kernel arguments, so no host buffer has to outlive the call and nothing
+// is copied through pageable memory.  Its first 30 KB ride with the score
+// statistics launch; this kernel carries the rest (no launch for the shapes
+// seen in practice).
 #include "vc_device.h"
 #include "vc_internal.h"
 
 namespace vc {
 
 namespace {
-
-// Payload sizes: the launch copies the whole argument block, so the smallest
-// one that holds the plan is used.
-constexpr uint32_t kSmallWords = 480, kMidWords = 2040, kBigWords = 7680;  // 1.9 / 8 / 30 KB
-
-template <uint32_t W>
-struct UploadChunk {
-  uint32_t words;
-  uint32_t pad;
-  uint32_t data[W];
-};
 
 template <uint32_t W>
 __global__ __launch_bounds__(256) void k_upload(uint32_t *dst, UploadChunk<W> c) {
@@ -40,17 +30,16 @@ hipError_t upload_chunk(uint32_t *dst, const uint8_t *src, uint32_t words, hipSt
 
 }  // namespace
 
-hipError_t launch_upload(uint8_t *dst, const uint8_t *src, size_t bytes, uint32_t * /*zero*/,
-                         size_t /*zero_words*/, hipStream_t st) {
+hipError_t launch_upload(uint8_t *dst, const uint8_t *src, size_t bytes, hipStream_t st) {
   // `bytes` is a multiple of 4 (the plan is built from 4- and 8-byte fields).
   const size_t words = bytes / 4;
-  for (size_t w0 = 0; w0 < words; w0 += kBigWords) {
-    const uint32_t n = (uint32_t)((words - w0) < (size_t)kBigWords ? (words - w0) : kBigWords);
+  for (size_t w0 = 0; w0 < words; w0 += kChunkWords) {
+    const uint32_t n = (uint32_t)((words - w0) < (size_t)kChunkWords ? (words - w0) : kChunkWords);
     uint32_t *d = reinterpret_cast<uint32_t *>(dst) + w0;
     const uint8_t *s = src + w0 * 4;
-    const hipError_t e = n <= kSmallWords ? upload_chunk<kSmallWords>(d, s, n, st)
-                         : n <= kMidWords ? upload_chunk<kMidWords>(d, s, n, st)
-                                          : upload_chunk<kBigWords>(d, s, n, st);
+    const hipError_t e = n <= kChunkWordsSmall ? upload_chunk<kChunkWordsSmall>(d, s, n, st)
+                         : n <= kChunkWordsMid ? upload_chunk<kChunkWordsMid>(d, s, n, st)
+                                               : upload_chunk<kChunkWords>(d, s, n, st);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

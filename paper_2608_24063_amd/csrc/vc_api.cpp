@@ -42,6 +42,11 @@ vc_status check_shape(const vc_shape *s) {
   if ((int64_t)(s->Hq / s->Hkv) * s->W > 1024) return VC_ERR_UNSUPPORTED;
   for (int32_t b = 0; b < s->B; ++b)
     if (s->n_vis[b] < 0 || s->n_vis[b] > kMaxTokens) return s->n_vis[b] < 0 ? VC_ERR_SHAPE : VC_ERR_UNSUPPORTED;
+  // The layer pointers, token offsets and lengths must fit the plan's first
+  // chunk (L = 128 layers leave room for about 1800 sequences).
+  if (sizeof(uint64_t) * (LP_COUNT * (size_t)s->L + s->B + 1) + sizeof(int32_t) * (size_t)s->B + 8 >
+      sizeof(uint32_t) * (size_t)kChunkWords)
+    return VC_ERR_UNSUPPORTED;
   return VC_OK;
 }
 
@@ -168,11 +173,14 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
 
   // Plan blob.
   size_t o = 0;
+  // The score statistics kernel reads the first three tables from the
+  // plan's first chunk, so they come first (check_shape bounds their size).
   y.p_lp = o; o += sizeof(uint64_t) * LP_COUNT * y.L;
   y.p_toff = o; o += sizeof(int64_t) * (y.B + 1);
+  y.p_nb = o; o += sizeof(int32_t) * y.B;
+  o = (o + 7) & ~size_t(7);
   y.p_orow = o; o += sizeof(int64_t) * y.L * (y.B + 1);
   y.p_drow = o; o += sizeof(int64_t) * y.L * (y.B + 1);
-  y.p_nb = o; o += sizeof(int32_t) * y.B;
   y.p_kk = o; o += sizeof(int32_t) * y.B * y.L;
   y.p_ns = o; o += sizeof(int32_t) * y.B * y.L;
   o = (o + 15) & ~size_t(15);
@@ -338,6 +346,9 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   pl.tc = (float)(1.4426950408889634 / (double)params->tau);
   pl.mu = params->mu;
   pl.Ntot = y.Ntot;
+  pl.w_lp = (int32_t)(y.p_lp / 4);
+  pl.w_toff = (int32_t)(y.p_toff / 4);
+  pl.w_nb = (int32_t)(y.p_nb / 4);
   uint8_t *pb = ws + y.off_plan;
   pl.lp = reinterpret_cast<const uint64_t *>(pb + y.p_lp);
   pl.nb = reinterpret_cast<const int32_t *>(pb + y.p_nb);
@@ -359,10 +370,16 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   auto mark = [&](int i) {
     return events && events[i] ? hipEventRecord(static_cast<hipEvent_t>(events[i]), hs) : hipSuccess;
   };
+  // The plan's first chunk travels with the score statistics launch; only a
+  // plan larger than one chunk needs upload launches for the rest.
+  const size_t first = std::min(blob.size(), sizeof(uint32_t) * (size_t)kChunkWords);
   if (mark(0) != hipSuccess) return VC_ERR_HIP;
-  if (launch_upload(pb, blob.data(), blob.size(), nullptr, 0, hs) != hipSuccess) return VC_ERR_HIP;
+  if (blob.size() > first && launch_upload(pb + first, blob.data() + first, blob.size() - first, hs) != hipSuccess)
+    return VC_ERR_HIP;
   if (mark(1) != hipSuccess) return VC_ERR_HIP;
-  if (launch_score_stats(pl, hs) != hipSuccess) return VC_ERR_HIP;
+  if (launch_score_stats(pl, reinterpret_cast<uint32_t *>(pb), blob.data(), (uint32_t)(first / 4), hs) !=
+      hipSuccess)
+    return VC_ERR_HIP;
   if (mark(2) != hipSuccess) return VC_ERR_HIP;
   if (launch_score_colsum(pl, hs) != hipSuccess) return VC_ERR_HIP;
   if (mark(3) != hipSuccess) return VC_ERR_HIP;

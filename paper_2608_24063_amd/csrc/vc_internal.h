@@ -33,8 +33,20 @@ struct FuseUnit {
 };
 static_assert(sizeof(FuseUnit) == 64, "fusion unit record is four 16-byte words");
 
+// The plan travels to the device as kernel arguments, in chunks of at most
+// kChunkWords words: the first with the score statistics launch (which
+// copies it into the workspace and reads its own tables from it), any
+// further ones with upload launches.
+constexpr uint32_t kChunkWordsSmall = 480, kChunkWordsMid = 2040, kChunkWords = 7680;  // 1.9 / 8 / 30 KB
+template <uint32_t W>
+struct UploadChunk {
+  uint32_t words;
+  uint32_t pad;
+  uint32_t data[W];
+};
+
 // Everything the prune kernels need, by value (a few hundred bytes).  Array
-// members point into the device workspace, filled by the plan upload kernel.
+// members point into the device workspace, filled from the plan chunks.
 struct PrunePlan {
   int32_t B, L, Hq, Hkv, d, W, G, R;
   int32_t h;          // truncation layer: layers [0, h) keep tokens
@@ -51,6 +63,7 @@ struct PrunePlan {
   float tc;           // log2(e) / tau
   float mu;
   int64_t Ntot;       // sum_b n_b
+  int32_t w_lp, w_toff, w_nb;  // word offsets of those tables in the plan (first chunk)
   const uint64_t *lp;   // [LP_COUNT][L] per-layer device pointers
   const int32_t *nb;    // [B]
   const int64_t *toff;  // [B+1] token offsets
@@ -70,9 +83,11 @@ struct PrunePlan {
 };
 
 // Host-side launchers (each returns hipSuccess or the launch error).
-hipError_t launch_upload(uint8_t *dst, const uint8_t *src, size_t bytes, uint32_t *zero,
-                         size_t zero_words, hipStream_t st);
-hipError_t launch_score_stats(const PrunePlan &p, hipStream_t st);
+hipError_t launch_upload(uint8_t *dst, const uint8_t *src, size_t bytes, hipStream_t st);
+// Score statistics; also writes the plan's first chunk (src, words <=
+// kChunkWords) to dst.
+hipError_t launch_score_stats(const PrunePlan &p, uint32_t *dst, const uint8_t *src, uint32_t words,
+                              hipStream_t st);
 hipError_t launch_score_colsum(const PrunePlan &p, hipStream_t st);
 hipError_t launch_score_global(const PrunePlan &p, hipStream_t st);
 hipError_t launch_select(const PrunePlan &p, hipStream_t st);
