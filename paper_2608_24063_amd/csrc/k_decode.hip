@@ -179,13 +179,17 @@ __device__ __forceinline__ uint64_t floor_div64(uint64_t a, uint32_t b) {
 // not change during a call, so every workgroup derives the same cut, and a
 // unit's length is read only by its own pieces, the last of which advances it
 // (no grid-wide ordering is needed).  The piece bound c is the smallest of
-// four multiples of 4 tiles (from T / grid up) whose piece count fits the
-// grid, so the four waves of a workgroup get equal numbers of tiles; if none
+// four multiples of 4 tiles (from T / grid up, at least kMinPiece: below
+// that, splitting a unit saves less than the merge of its pieces costs) whose
+// piece count fits the grid, so the four waves of a workgroup get equal
+// numbers of tiles; if none
 // fits, c = T / (grid - U) (rounded up to a multiple of 4) always does, since
 // the pieces then number at most T / c + U.  Each wave computes the whole cut
 // by itself (lane l takes units 64 k + l of each 256-unit chunk), so no
 // barrier is needed; the result, this workgroup's piece, is the same in every
 // wave.
+constexpr uint32_t kMinPiece = kDecodeMinPiece;
+
 struct Piece {
   int32_t u, j, np, p0, nt, len0, cap;  // u = -1: no piece
   int64_t roff;                         // the unit's first pool row
@@ -224,7 +228,7 @@ __device__ __forceinline__ Piece cut(const DecodePlan &p, uint32_t i) {
     T += wave_sum(tl[0] + tl[1] + tl[2] + tl[3]);
   }
   const uint32_t N = gridDim.x;  // > U (host)
-  const uint32_t c0 = max(4u, (T / N + (T % N != 0) + 3u) & ~3u);
+  const uint32_t c0 = max(kMinPiece, (T / N + (T % N != 0) + 3u) & ~3u);
   const bool small = T + c0 + 16u < (1u << 20);
   Recip rc[4];
 #pragma unroll

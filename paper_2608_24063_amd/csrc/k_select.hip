@@ -62,12 +62,17 @@ __global__ __launch_bounds__(kThreads) void k_select(PrunePlan p) {
   const int g = u % p.Hkv;
   const int b = (u / p.Hkv) % p.B;
   const int l = u / (p.Hkv * p.B);
+  // Every parameter of the unit, output pointers included, in one batch of
+  // loads.  There is no early exit: a unit with n_surv = 0 (k = 0) finds no
+  // kept or dropped token below and writes nothing, and without the branch
+  // the loads are not deferred behind the first one.
   const int nsv = ldg(p.ns + b * p.L + l);
-  if (nsv == 0) return;
   const int n = ldg(p.nb + b);
   const int k = ldg(p.kk + b * p.L + l);
-  const int r = nsv - k;
   const int64_t toff = ldg(p.toff + b);
+  const uint64_t idx_base = ldg(p.lp + LP_IDX * p.L + l), drop_base = ldg(p.lp + LP_DROP * p.L + l);
+  const int64_t orow = ldg(p.orow + l * (p.B + 1) + b), drow = ldg(p.drow + l * (p.B + 1) + b);
+  const int r = nsv - k;
 
   const float *S = p.mode ? p.gs + toff
                           : p.S + (int64_t)l * p.Ntot * p.Hkv + toff * p.Hkv + (int64_t)g * n;
@@ -152,10 +157,8 @@ __global__ __launch_bounds__(kThreads) void k_select(PrunePlan p) {
   const uint32_t c2[4] = {nkeep, ndrop, 0, 0};
   block_scan4<kWaves>(c2, ex, tot4, wt);
 
-  int32_t *idx = reinterpret_cast<int32_t *>(ldg(p.lp + LP_IDX * p.L + l)) +
-                 ldg(p.orow + l * (p.B + 1) + b) + (int64_t)g * k;
-  int32_t *drop = reinterpret_cast<int32_t *>(ldg(p.lp + LP_DROP * p.L + l)) +
-                  ldg(p.drow + l * (p.B + 1) + b) + (int64_t)g * r;
+  int32_t *idx = reinterpret_cast<int32_t *>(idx_base) + orow + (int64_t)g * k;
+  int32_t *drop = reinterpret_cast<int32_t *>(drop_base) + drow + (int64_t)g * r;
   uint32_t pk = ex[0], pd = ex[1];
 #pragma unroll
   for (int i = 0; i < PER; ++i) {

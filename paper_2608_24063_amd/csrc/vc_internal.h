@@ -98,19 +98,20 @@ hipError_t launch_fuse(const PrunePlan &p, hipStream_t st);
 // size).
 constexpr int kDecodeTileRows = 32;
 constexpr int kDecodeSlots = 512;  // resident decode workgroups (256 CUs x 2)
+constexpr int kDecodeMinPiece = 8; // smallest piece bound in tiles (a multiple of 4)
 
 // Workgroups of a decode launch over `units` caches of at most max_rows rows:
 // the resident slots (more for many units: each unit takes at least one
-// piece), at most the pieces of 4 tiles the rows can form, and always more
-// than `units`, which the device's fallback piece size relies on.  0 if the
-// tile count of the bound does not fit 31 bits.
+// piece), at most the pieces of kDecodeMinPiece tiles the rows can form, and
+// always more than `units`, which the device's fallback piece size relies
+// on.  0 if the tile count of the bound does not fit 31 bits.
 inline int32_t decode_grid(int64_t units, int64_t max_rows) {
   if (units < 1 || max_rows < 0 || max_rows > (int64_t(1) << 40)) return 0;
   const int64_t per = max_rows == 0 ? 1 : (max_rows + kDecodeTileRows - 1) / kDecodeTileRows;
   if (per > ((int64_t(1) << 31) - 1) / units) return 0;
   int64_t n = units + kDecodeSlots / 2;
   if (n < kDecodeSlots) n = kDecodeSlots;
-  const int64_t most = units * ((per + 3) / 4);
+  const int64_t most = units * ((per + kDecodeMinPiece - 1) / kDecodeMinPiece);
   if (n > most) n = most;
   if (n < units + 1) n = units + 1;
   return n > INT32_MAX ? 0 : (int32_t)n;
