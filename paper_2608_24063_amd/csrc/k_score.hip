@@ -393,22 +393,43 @@ __global__ __launch_bounds__(256, 3) void k_score_colsum(PrunePlan p) {
   }
 }
 
-// Shared ranking: s[v] = sum over all layers and kv heads of S, in fixed
-// (layer, head) order, accumulated in fp64.
+// Shared ranking: s[v] = sum over all layers and kv heads of S, accumulated
+// in fp64 in a fixed order: wave w sums the w-th quarter of the (layer,
+// head) pairs in order, loading 16 at a time, and the quarters are added in
+// order.  A workgroup covers 64 consecutive tokens, so every load of a wave
+// reads one contiguous run.
 __global__ __launch_bounds__(256) void k_score_global(PrunePlan p) {
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= p.Ntot) return;
+  __shared__ double part[4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t t = (int64_t)blockIdx.x * 64 + lane;
+  const bool in = t < p.Ntot;
+  const int64_t tc = in ? t : p.Ntot - 1;
+  // Sequence of token tc: the number of later sequence starts at or before it
+  // (independent loads; empty sequences are passed over).
   int b = 0;
-  while (b + 1 < p.B && ldg(p.toff + b + 1) <= t) ++b;
+  for (int bb = 1; bb < p.B; ++bb) b += ldg(p.toff + bb) <= tc ? 1 : 0;
   const int64_t toff = ldg(p.toff + b);
-  const int64_t v = t - toff;
+  const int64_t v = tc - toff;
   const int n = ldg(p.nb + b);
+  const float *S = p.S + toff * p.Hkv + v;
+  const int npair = p.Ls * p.Hkv;
+  const int q0 = npair * w / 4, q1 = npair * (w + 1) / 4;
   double acc = 0.0;
-  for (int l = 0; l < p.Ls; ++l) {
-    const float *S = p.S + (int64_t)l * p.Ntot * p.Hkv + toff * p.Hkv;
-    for (int g = 0; g < p.Hkv; ++g) acc += (double)ldg(S + (int64_t)g * n + v);
+  for (int q = q0; q < q1; q += 16) {
+    float x[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int qq = min(q + i, q1 - 1);
+      const int l = qq / p.Hkv, g = qq - l * p.Hkv;
+      x[i] = ldg(S + (int64_t)l * p.Ntot * p.Hkv + (int64_t)g * n);
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (q + i < q1) acc += (double)x[i];
   }
-  stg(p.gs + t, (float)acc);
+  part[w][lane] = acc;
+  __syncthreads();
+  if (w == 0 && in) stg(p.gs + t, (float)(((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane]));
 }
 
 }  // namespace
@@ -451,7 +472,7 @@ hipError_t launch_score_colsum(const PrunePlan &p, hipStream_t st) {
 }
 
 hipError_t launch_score_global(const PrunePlan &p, hipStream_t st) {
-  const uint32_t grid = (uint32_t)((p.Ntot + 255) / 256);
+  const uint32_t grid = (uint32_t)((p.Ntot + 63) / 64);
   if (grid == 0) return hipSuccess;
   hipLaunchKernelGGL(k_score_global, dim3(grid), dim3(256), 0, st, p);
   return hipGetLastError();
