@@ -39,6 +39,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="vllm7b")
     ap.add_argument("--rank-mode", default="layer_head", choices=["layer_head", "global"])
+    ap.add_argument("--schedule", default="parabolic", choices=["parabolic", "fixed", "arithmetic", "geometric"],
+                    help="layer budget schedule (the budget ablation's alternatives to the parabola)")
+    ap.add_argument("--drop-all", action="store_true", help="fuse every non-kept token (n_surv = n)")
     ap.add_argument("--decode-steps", type=int, default=None)
     ap.add_argument("--no-flush", action="store_true", help="keep caches warm between steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -382,7 +385,9 @@ def main():
           file=sys.stderr, flush=True)
     keep_host = not args.no_cpu_baseline
     dv, host = upload_layers(w, range(w.L), dev, keep_host=keep_host)
-    params = vc.make_params(w.retention, rank_mode=mode)
+    sched = {"parabolic": vc.VC_SCHED_PARABOLIC, "fixed": vc.VC_SCHED_FIXED,
+             "arithmetic": vc.VC_SCHED_ARITHMETIC, "geometric": vc.VC_SCHED_GEOMETRIC}[args.schedule]
+    params = vc.make_params(w.retention, rank_mode=mode, schedule=sched, drop_all=args.drop_all)
     pc = PruneCall(w.B, w.L, w.Hq, w.Hkv, w.d, w.W, n, params, [dv["K"][l] for l in range(w.L)],
                    [dv["V"][l] for l in range(w.L)], [dv["Q"][l] for l in range(w.L)])
     # Flush by reading (not writing) 1 GiB, so the caches hold clean lines and
@@ -437,7 +442,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{w.name}: B={w.B} L={w.L} Hq={w.Hq} Hkv={w.Hkv} d={w.d} "
                                f"{w.frames}x{w.tokens_per_frame} visual tokens, W={w.W}, RR={w.retention}",
-                   "rank_mode": args.rank_mode, "cold_caches": flush is not None,
+                   "rank_mode": args.rank_mode, "schedule": args.schedule, "drop_all": args.drop_all,
+                   "cold_caches": flush is not None,
                    "input_visual_kv_bytes": in_bytes},
         "hbm_frac_path": alg["path_bytes"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "path_alg_bytes": alg["path_bytes"],

@@ -51,9 +51,26 @@ typedef enum {
  *               kv heads; every layer and head keeps the top-k_l of it. */
 typedef enum { VC_RANK_LAYER_HEAD = 0, VC_RANK_GLOBAL = 1 } vc_rank_mode;
 
+/* Layer budget schedule: the proportions b_l, l = 1..h, before they are
+ * normalised to h*m.  PARABOLIC is PruneKV's Eq. (parabolic); the others are
+ * the alternatives of the budget ablation (Sec. 5, Table "Ablation study on
+ * budget allocation strategy"), whose constants the paper leaves open:
+ *   FIXED:      b_l = 1 (uniform);
+ *   ARITHMETIC: linear from b_1 = 1 to b_h = 1/2 (the raw parabola's
+ *               endpoints), b_l = 1 - (l-1) / (2 (h-1));
+ *   GEOMETRIC:  layers 1..h in four equal depth blocks, block j (0-based,
+ *               j = floor(4 (l-1) / h)) gets b_l = 2^-j. */
+typedef enum {
+  VC_SCHED_PARABOLIC = 0,
+  VC_SCHED_FIXED = 1,
+  VC_SCHED_ARITHMETIC = 2,
+  VC_SCHED_GEOMETRIC = 3
+} vc_schedule;
+
 /* Method parameters.  Defaults (viscache_default_params) are the paper's fixed
  * hyper-parameters from Sec. 4, Implementation Details: h = 3/4 L, m = 0.75,
- * tau = 1.0, mu = 0.7. */
+ * tau = 1.0, mu = 0.7, the parabolic schedule, fusion of the top-q
+ * survivors. */
 typedef struct {
   double retention; /* overall retention ratio RR in (0, 1]; RR = q*(h/L)*m, so
                        the token-level ratio is q = RR / ((h/L) m), and q > 1 is
@@ -67,6 +84,12 @@ typedef struct {
   float mu;         /* fusion weight of Eq. (weight_fusion), in [0, 1] */
   int32_t rank_mode;  /* vc_rank_mode */
   int32_t v_out_fp32; /* 0: fused values stored as bf16; 1: stored as fp32 */
+  int32_t schedule;   /* vc_schedule */
+  int32_t drop_all;   /* 0: the dropped tokens whose values are fused are the
+                         survivors of the top-q cut outside the kept set
+                         (Algorithm 1, n_surv = min(n, max(round(q n), k_1)));
+                         1: every token outside the kept set (n_surv = n),
+                         the reading of Eq. (redistribution) alone. */
 } vc_params;
 
 /* Problem shape.  L layers, Hq query heads, Hkv kv heads (Hq % Hkv == 0;
@@ -83,8 +106,8 @@ typedef struct {
 /* Fill *p with the defaults above and the given retention. */
 void viscache_default_params(vc_params *p, double retention);
 
-/* Host only.  Layer budgets, Eq. (parabolic) normalised to h*m, and the
- * top-q survivor count of Algorithm 1 Step 1:
+/* Host only.  Layer budgets (the schedule normalised to h*m; Eq.
+ * (parabolic) by default) and the survivor count of Algorithm 1 Step 1:
  *   k[b*L + l]      tokens kept in layer l of sequence b (0 for l >= h),
  *   n_surv[b*L + l] tokens that survive the top-q cut (same for every l),
  *   *h_out          the truncation layer used (may be NULL).

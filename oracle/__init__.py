@@ -47,7 +47,7 @@ def lib():
             path = _LIB if os.path.exists(_LIB) else build()
             L = ctypes.CDLL(path)
             vp, i32, f64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_double
-            L.orc_budget.argtypes = [i32, i32, f64, i32, f64, P_i32, P_i32, P_i32, P_f64, P_f64]
+            L.orc_budget.argtypes = [i32, i32, f64, i32, f64, i32, i32, P_i32, P_i32, P_i32, P_f64, P_f64]
             L.orc_budget.restype = ctypes.c_int
             L.orc_scores_unit.argtypes = [i32, i32, i32, vp, vp, vp]
             L.orc_select.argtypes = [i32, vp, i32, i32, vp, vp]
@@ -65,12 +65,15 @@ def _p(a: np.ndarray):
     return a.ctypes.data
 
 
-def budget(L: int, n: int, rr: float, h: int = 0, m: float = 0.75):
+SCHEDULES = {"parabolic": 0, "fixed": 1, "arithmetic": 2, "geometric": 3}
+
+
+def budget(L: int, n: int, rr: float, h: int = 0, m: float = 0.75, schedule: int = 0, drop_all: bool = False):
     """Returns dict(k=int32[L], n_surv, h, b=float64[L], q) or raises ValueError."""
     k = np.zeros(L, dtype=np.int32)
     b = np.zeros(L, dtype=np.float64)
     ns, ho, q = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_double()
-    rc = lib().orc_budget(L, n, rr, h, m, k.ctypes.data_as(P_i32), ctypes.byref(ns),
+    rc = lib().orc_budget(L, n, rr, h, m, int(schedule), int(drop_all), k.ctypes.data_as(P_i32), ctypes.byref(ns),
                           ctypes.byref(ho), b.ctypes.data_as(P_f64), ctypes.byref(q))
     if rc != 0:
         raise ValueError("invalid budget parameters")

@@ -45,7 +45,7 @@ static int frac_cmp(const void *a, const void *b) {
   return x->layer < y->layer ? -1 : (x->layer > y->layer); /* tie: lower layer */
 }
 
-int orc_budget(int32_t L, int32_t n, double rr, int32_t h_param, double m,
+int orc_budget(int32_t L, int32_t n, double rr, int32_t h_param, double m, int32_t schedule, int32_t drop_all,
                int32_t *k, int32_t *n_surv, int32_t *h_out, double *b_out, double *q_out) {
   if (L < 2 || n < 0) return -1;
   if (!(rr > 0.0 && rr <= 1.0) || !(m > 0.0 && m <= 1.0)) return -1;
@@ -53,13 +53,31 @@ int orc_budget(int32_t L, int32_t n, double rr, int32_t h_param, double m,
   int32_t h = h_param ? h_param : (int32_t)floor(0.75 * (double)L + 0.5);
   if (h < 2 || h > L) return -1;
 
-  /* Raw parabola: b_l = 1 - (l-1)^2 / (2 (h-1)^2), l = 1..h (b_1 = 1, b_h = 1/2). */
+  if (schedule < 0 || schedule > 3) return -1;
+  /* Raw proportions, l = 1..h.
+   *   0 parabola (Eq. parabolic): b_l = 1 - (l-1)^2 / (2 (h-1)^2), b_1 = 1, b_h = 1/2;
+   *   1 fixed (budget ablation, "uniform budget per layer"): b_l = 1;
+   *   2 arithmetic (ablation, linear progression; reading: the parabola's
+   *     endpoints 1 and 1/2): b_l = 1 - (l-1) / (2 (h-1));
+   *   3 geometric (ablation, progression over four layer blocks; reading:
+   *     equal depth blocks, ratio 1/2): b_l = 2^-floor(4 (l-1) / h). */
   double *raw = (double *)malloc(sizeof(double) * (size_t)h);
   double *b = (double *)malloc(sizeof(double) * (size_t)h);
   for (int32_t l = 1; l <= h; ++l) {
-    double num = (double)(l - 1) * (double)(l - 1);
-    double den = 2.0 * (double)(h - 1) * (double)(h - 1);
-    raw[l - 1] = 1.0 - num / den;
+    if (schedule == 0) {
+      double num = (double)(l - 1) * (double)(l - 1);
+      double den = 2.0 * (double)(h - 1) * (double)(h - 1);
+      raw[l - 1] = 1.0 - num / den;
+    } else if (schedule == 1) {
+      raw[l - 1] = 1.0;
+    } else if (schedule == 2) {
+      raw[l - 1] = 1.0 - (double)(l - 1) / (2.0 * (double)(h - 1));
+    } else {
+      int32_t block = (4 * (l - 1)) / h;
+      double v = 1.0;
+      for (int32_t j = 0; j < block; ++j) v *= 0.5;
+      raw[l - 1] = v;
+    }
   }
   /* Normalise so that sum_l b_l = h*m.  Reading: a common scale factor, with
    * any proportion that would exceed 1 held at 1 and the remaining target
@@ -111,10 +129,13 @@ int orc_budget(int32_t L, int32_t n, double rr, int32_t h_param, double m,
   for (int32_t i = h; i < L; ++i) k[i] = 0; /* layers beyond h are evicted */
   for (int32_t i = 0; i < h; ++i) if (k[i] > n) bad = 1;
 
-  /* Survivors of the top-q cut; never fewer than the largest layer budget. */
+  /* Survivors of the top-q cut; never fewer than the largest layer budget.
+   * With drop_all every token survives: the values of all non-kept tokens
+   * are fused (Eq. (redistribution) read on its own). */
   int32_t ns = (int32_t)floor(q * (double)n + 0.5);
-  if (ns < k[0]) ns = k[0];
+  for (int32_t i = 0; i < h; ++i) if (ns < k[i]) ns = k[i];
   if (ns > n) ns = n;
+  if (drop_all) ns = n;
   *n_surv = ns;
   if (h_out) *h_out = h;
   if (q_out) *q_out = q;

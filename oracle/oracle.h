@@ -22,11 +22,14 @@ extern "C" {
  * follows it, the retention-ratio composition RR = p*q*(h/L)*m of the
  * implementation details (p = 1), and Alg. 1 Step 1 (the top-q cut).
  * Inputs: L layers, n visual tokens, overall retention rr in (0,1], h_param
- * (0 selects round(0.75 L)), mean budget m in (0,1].
+ * (0 selects round(0.75 L)), mean budget m in (0,1], schedule (0 parabola,
+ * 1 fixed, 2 arithmetic, 3 geometric: the budget ablation's alternatives to
+ * Eq. (parabolic)), drop_all (1: every token survives, so every non-kept
+ * token is fused).
  * Outputs: k[L] kept tokens per layer (0 beyond h), *n_surv (tokens that
  * survive the top-q cut), *h_out, b_out[L] (normalised proportions, may be
  * NULL), *q_out (may be NULL).  Returns 0, or -1 on invalid parameters. */
-int orc_budget(int32_t L, int32_t n, double rr, int32_t h_param, double m,
+int orc_budget(int32_t L, int32_t n, double rr, int32_t h_param, double m, int32_t schedule, int32_t drop_all,
                int32_t *k, int32_t *n_surv, int32_t *h_out, double *b_out, double *q_out);
 
 /* Window score of one (sequence, layer, kv head) unit, Eq. (token_score) read

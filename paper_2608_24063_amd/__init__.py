@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(HERE, "libviscache.so")
 
 VC_OK, VC_ERR_ARG, VC_ERR_SHAPE, VC_ERR_BUDGET, VC_ERR_WORKSPACE, VC_ERR_UNSUPPORTED, VC_ERR_HIP = range(7)
 VC_RANK_LAYER_HEAD, VC_RANK_GLOBAL = 0, 1
+VC_SCHED_PARABOLIC, VC_SCHED_FIXED, VC_SCHED_ARITHMETIC, VC_SCHED_GEOMETRIC = 0, 1, 2, 3
 
 P = ctypes.POINTER
 c_i32, c_i64, c_f32, c_f64, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_void_p
@@ -23,7 +24,7 @@ c_i32, c_i64, c_f32, c_f64, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_floa
 
 class vc_params(ctypes.Structure):
     _fields_ = [("retention", c_f64), ("h", c_i32), ("m", c_f64), ("tau", c_f32), ("mu", c_f32),
-                ("rank_mode", c_i32), ("v_out_fp32", c_i32)]
+                ("rank_mode", c_i32), ("v_out_fp32", c_i32), ("schedule", c_i32), ("drop_all", c_i32)]
 
 
 class vc_shape(ctypes.Structure):
@@ -102,10 +103,12 @@ def _check(status: int, what: str) -> None:
 # ---- parameter / shape construction -----------------------------------------
 
 def make_params(retention: float, h: int = 0, m: float = 0.75, tau: float = 1.0, mu: float = 0.7,
-                rank_mode: int = VC_RANK_LAYER_HEAD, v_out_fp32: bool = False) -> vc_params:
+                rank_mode: int = VC_RANK_LAYER_HEAD, v_out_fp32: bool = False,
+                schedule: int = VC_SCHED_PARABOLIC, drop_all: bool = False) -> vc_params:
     p = vc_params()
     lib().viscache_default_params(ctypes.byref(p), retention)
     p.h, p.m, p.tau, p.mu, p.rank_mode, p.v_out_fp32 = h, m, tau, mu, rank_mode, int(v_out_fp32)
+    p.schedule, p.drop_all = int(schedule), int(drop_all)
     return p
 
 

@@ -59,6 +59,8 @@ vc_status check_params(const vc_params *p, int32_t L) {
   if (!(p->mu >= 0.f && p->mu <= 1.f)) return VC_ERR_ARG;
   if (p->rank_mode != VC_RANK_LAYER_HEAD && p->rank_mode != VC_RANK_GLOBAL) return VC_ERR_ARG;
   if (p->v_out_fp32 != 0 && p->v_out_fp32 != 1) return VC_ERR_ARG;
+  if (p->schedule < VC_SCHED_PARABOLIC || p->schedule > VC_SCHED_GEOMETRIC) return VC_ERR_ARG;
+  if (p->drop_all != 0 && p->drop_all != 1) return VC_ERR_ARG;
   return VC_OK;
 }
 
@@ -78,7 +80,8 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   y.h = 0;
   for (int32_t b = 0; b < y.B; ++b) {
     int32_t nsv = 0, hu = 0;
-    if (!budget_one(y.L, y.n[b], p->retention, p->h, p->m, &y.k[(size_t)b * y.L], &nsv, &hu))
+    if (!budget_one(y.L, y.n[b], p->retention, p->h, p->m, p->schedule, p->drop_all, &y.k[(size_t)b * y.L],
+                    &nsv, &hu))
       return VC_ERR_BUDGET;
     for (int32_t l = 0; l < y.L; ++l) y.ns[(size_t)b * y.L + l] = nsv;
     y.h = hu;
@@ -215,6 +218,8 @@ void viscache_default_params(vc_params *p, double retention) {
   p->mu = 0.7f;
   p->rank_mode = VC_RANK_LAYER_HEAD;
   p->v_out_fp32 = 0;
+  p->schedule = VC_SCHED_PARABOLIC;
+  p->drop_all = 0;
 }
 
 vc_status viscache_budget(const vc_shape *shape, const vc_params *params, int32_t *k,

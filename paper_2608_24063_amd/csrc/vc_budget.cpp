@@ -1,6 +1,8 @@
 // vc_budget.cpp -- layer budgets of PruneKV on the host (Sec. 3.2, Eq.
 // (parabolic) and the normalisation sum_{l<=h} b_l = h*m; Sec. 4, RR =
 // p*q*(h/L)*m with p = 1; Algorithm 1, Step 1 for the top-q survivors).
+// The fixed, arithmetic and geometric schedules of the budget ablation
+// replace only the raw proportions (readings stated in viscache.h).
 //
 // Integer rule (a reading; the paper gives proportions only): the per-sequence
 // total T = floor(RR*L*n + 0.5) is apportioned to layers 1..h in proportion to
@@ -16,8 +18,8 @@
 
 namespace vc {
 
-bool budget_one(int32_t L, int32_t n, double rr, int32_t h_param, double m, int32_t *k,
-                int32_t *n_surv, int32_t *h_used) {
+bool budget_one(int32_t L, int32_t n, double rr, int32_t h_param, double m, int32_t schedule, int32_t drop_all,
+                int32_t *k, int32_t *n_surv, int32_t *h_used) {
   if (L < 2 || n < 0) return false;
   if (!(rr > 0.0 && rr <= 1.0) || !(m > 0.0 && m <= 1.0)) return false;
   const int32_t h = h_param != 0 ? h_param : static_cast<int32_t>(std::floor(0.75 * L + 0.5));
@@ -27,7 +29,22 @@ bool budget_one(int32_t L, int32_t n, double rr, int32_t h_param, double m, int3
   const double den = 2.0 * static_cast<double>(h - 1) * static_cast<double>(h - 1);
   for (int32_t i = 0; i < h; ++i) {
     const double li = static_cast<double>(i);  // l - 1
-    raw[i] = 1.0 - (li * li) / den;
+    switch (schedule) {
+      case 0:  // parabolic
+        raw[i] = 1.0 - (li * li) / den;
+        break;
+      case 1:  // fixed
+        raw[i] = 1.0;
+        break;
+      case 2:  // arithmetic, 1 down to 1/2
+        raw[i] = 1.0 - li / (2.0 * static_cast<double>(h - 1));
+        break;
+      case 3:  // geometric over four depth blocks
+        raw[i] = std::ldexp(1.0, -static_cast<int>((4 * i) / h));
+        break;
+      default:
+        return false;
+    }
   }
   // Water filling towards sum = h*m.
   std::vector<bool> held(h, false);
@@ -80,8 +97,9 @@ bool budget_one(int32_t L, int32_t n, double rr, int32_t h_param, double m, int3
     if (k[i] > n) return false;
 
   int32_t ns = static_cast<int32_t>(std::floor(q * static_cast<double>(n) + 0.5));
-  ns = std::max(ns, k[0]);
+  for (int32_t i = 0; i < h; ++i) ns = std::max(ns, k[i]);
   ns = std::min(ns, n);
+  if (drop_all) ns = n;
   *n_surv = ns;
   if (h_used) *h_used = h;
   return true;

@@ -37,17 +37,30 @@ def test_defaults_match_paper(vc):
     p = vc.make_params(0.28)
     assert (p.h, p.m, p.tau, p.mu, p.rank_mode, p.v_out_fp32) == (0, 0.75, pytest.approx(1.0),
                                                                     pytest.approx(0.7), 0, 0)
+    assert (p.schedule, p.drop_all) == (vc.VC_SCHED_PARABOLIC, 0)
 
 
+def test_schedule_and_drop_all_are_checked(vc):
+    shape = vc.make_shape(1, 4, 8, 2, 64, 4, [64])
+    for bad in (dict(schedule=4), dict(schedule=-1), dict(drop_all=2)):
+        p = vc.make_params(0.25)
+        for k, v in bad.items():
+            setattr(p, k, v)
+        with pytest.raises(vc.VisCacheError) as ei:
+            vc.viscache_budget(shape, p)
+        assert ei.value.status == vc.VC_ERR_ARG
+
+
+@pytest.mark.parametrize("schedule,drop_all", [(0, False), (1, False), (2, False), (3, False), (0, True)])
 @pytest.mark.parametrize("L", [2, 3, 4, 8, 28, 36, 64, 80])
-def test_budget_matches_oracle(vc, orc, L):
+def test_budget_matches_oracle(vc, orc, L, schedule, drop_all):
     for n in [0, 1, 7, 64, 511, 512, 3136, 12544, 23040]:
         for rr in [0.05, 0.19, 0.22, 0.25, 0.28, 0.40, 0.5625]:
             for m in [0.75, 0.9]:
                 shape = vc.make_shape(1, L, 8, 2, 64, 4, [n])
-                params = vc.make_params(rr, m=m)
+                params = vc.make_params(rr, m=m, schedule=schedule, drop_all=drop_all)
                 try:
-                    ref = orc.budget(L=L, n=n, rr=rr, m=m)
+                    ref = orc.budget(L=L, n=n, rr=rr, m=m, schedule=schedule, drop_all=drop_all)
                 except ValueError:
                     with pytest.raises(vc.VisCacheError) as ei:
                         vc.viscache_budget(shape, params)

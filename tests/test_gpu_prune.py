@@ -37,13 +37,14 @@ def _diag(rec):
 class Run:
     """One viscache_prune call on a seeded workload, with host copies."""
 
-    def __init__(self, w, dev, mode=0, vfp32=False, rr=None, h=0, m=0.75, tau=1.0, mu=0.7):
+    def __init__(self, w, dev, mode=0, vfp32=False, rr=None, h=0, m=0.75, tau=1.0, mu=0.7, schedule=0,
+                 drop_all=False):
         import paper_2608_24063_amd as vc
         from paper_2608_24063_amd.tensors import PruneCall
         from synthgen.device import to_host_bf16, upload_layers
         self.w, self.mode, self.vfp32, self.tau, self.mu = w, mode, vfp32, tau, mu
         self.params = vc.make_params(rr if rr is not None else w.retention, h=h, m=m, tau=tau, mu=mu,
-                                     rank_mode=mode, v_out_fp32=vfp32)
+                                     rank_mode=mode, v_out_fp32=vfp32, schedule=schedule, drop_all=drop_all)
         self.n = [int(x) for x in w.n_vis()]
         self.toff = np.concatenate([[0], np.cumsum(self.n)]).astype(np.int64)
         shape = vc.make_shape(w.B, w.L, w.Hq, w.Hkv, w.d, w.W, self.n)
@@ -280,6 +281,41 @@ def test_repeat_is_bitwise_deterministic(dev, sg):
 @pytest.fixture(scope="module")
 def run7b(dev, sg):
     return Run(sg.VLLM7B, dev)
+
+
+# ------------------------------------- budget ablation schedules, fuse-all
+def _budgets_match_oracle(r, orc, schedule=0, drop_all=False):
+    for b, nb in enumerate(r.n):
+        ref = orc.budget(L=r.w.L, n=nb, rr=r.w.retention, schedule=schedule, drop_all=drop_all)
+        assert list(r.k[b * r.w.L:(b + 1) * r.w.L]) == list(ref["k"])
+        assert r.ns[b * r.w.L] == ref["n_surv"]
+
+
+@pytest.mark.parametrize("schedule", [1, 2, 3])
+def test_tiny_alternative_schedules_full(dev, orc, sg, schedule):
+    """Fixed, arithmetic and geometric budgets (the budget ablation) through
+    the whole path, every unit against the oracle."""
+    r = Run(sg.TINY, dev, schedule=schedule, vfp32=True)
+    _budgets_match_oracle(r, orc, schedule=schedule)
+    swaps, ferr, serr = r.check_all_layer_head(orc, _all_units(r))
+    assert serr < 1e-4
+
+
+@pytest.mark.parametrize("vfp32", [False, True])
+def test_tiny_fuse_all_full(dev, orc, sg, vfp32):
+    """Every non-kept token fused (n_surv = n), every unit."""
+    r = Run(sg.TINY, dev, drop_all=True, vfp32=vfp32)
+    _budgets_match_oracle(r, orc, drop_all=True)
+    assert all(x == n for b, n in enumerate(r.n) for x in r.ns[b * r.w.L:(b + 1) * r.w.L])
+    r.check_all_layer_head(orc, _all_units(r))
+
+
+def test_vllm7b_fuse_all_sampled(dev, orc, sg):
+    """7B shape with every non-kept token fused: dropped lists of up to
+    n - k_h = 2430 rows per unit (38 tiles)."""
+    r = Run(sg.VLLM7B, dev, drop_all=True, vfp32=True)
+    _budgets_match_oracle(r, orc, drop_all=True)
+    r.check_all_layer_head(orc, [(0, 0, 0), (10, 0, 1), (r.h - 1, 0, 3)])
 
 
 def test_vllm7b_layer_head_full(run7b, orc):

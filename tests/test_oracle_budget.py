@@ -130,3 +130,72 @@ def test_workload_budgets(orc, sg):
         for n in w.n_vis():
             r = orc.budget(L=w.L, n=int(n), rr=w.retention)
             assert int(r["k"].sum()) == math.floor(w.retention * w.L * int(n) + 0.5)
+
+
+# ---- alternative schedules of the budget ablation and the fuse-all reading ----
+
+def test_fixed_schedule_is_uniform(orc):
+    # "Uniform budget per layer": every proportion equals m, and the integer
+    # budgets of layers 1..h differ by at most one token.
+    for L, n, rr in [(28, 3136, 0.28), (80, 8192, 0.22), (4, 512, 0.25)]:
+        r = orc.budget(L=L, n=n, rr=rr, schedule=orc.SCHEDULES["fixed"])
+        h = r["h"]
+        assert np.allclose(r["b"][:h], 0.75, rtol=0, atol=1e-15)
+        k = r["k"][:h]
+        assert k.max() - k.min() <= 1
+        assert k.sum() == math.floor(rr * L * n + 0.5)
+
+
+@pytest.mark.parametrize("h", [3, 21, 60])
+def test_arithmetic_schedule_is_linear_from_one_to_half(orc, h):
+    # Endpoints 1 and 1/2 make the mean exactly 0.75, so at m = 0.75 the
+    # normalisation leaves the line unchanged: equal steps, b_1 = 1, b_h = 1/2.
+    r = orc.budget(L=80, n=8192, rr=0.01, h=h, m=0.75, schedule=orc.SCHEDULES["arithmetic"])
+    b = r["b"][:h]
+    assert b[0] == pytest.approx(1.0, abs=1e-15) and b[-1] == pytest.approx(0.5, abs=1e-15)
+    steps = np.diff(b)
+    assert np.allclose(steps, steps[0], rtol=0, atol=1e-14) and steps[0] < 0
+    # Integer budgets follow: successive differences vary by at most one token
+    # around a constant step.
+    r = orc.budget(L=28, n=3136, rr=0.28, schedule=orc.SCHEDULES["arithmetic"])
+    dk = np.diff(r["k"][:r["h"]].astype(np.int64))
+    assert dk.max() - dk.min() <= 2 and np.all(dk <= 0)
+
+
+def test_geometric_schedule_water_fills_four_blocks(orc):
+    # Four equal depth blocks with ratio 1/2 give raw 1, 1/2, 1/4, 1/8 (mean
+    # 15/32 < 0.75): scaling to the mean 0.75 holds blocks 0 and 1 at 1 and
+    # leaves 2/3 and 1/3 for blocks 2 and 3 (the sum is h*m exactly).
+    h = 20
+    r = orc.budget(L=28, n=4000, rr=0.05, h=h, m=0.75, schedule=orc.SCHEDULES["geometric"])
+    b = r["b"][:h].reshape(4, 5)
+    for j, want in enumerate([1.0, 1.0, 2.0 / 3.0, 1.0 / 3.0]):
+        assert np.allclose(b[j], want, rtol=0, atol=1e-15)
+    assert b.sum() == pytest.approx(h * 0.75, rel=1e-14)
+
+
+@pytest.mark.parametrize("schedule", ["parabolic", "fixed", "arithmetic", "geometric"])
+def test_schedules_keep_the_integer_invariants(orc, schedule):
+    s = orc.SCHEDULES[schedule]
+    for L in [2, 4, 28, 80]:
+        for n in [0, 1, 64, 3136, 12544]:
+            for rr in [0.05, 0.19, 0.28]:
+                try:
+                    r = orc.budget(L=L, n=n, rr=rr, schedule=s)
+                except ValueError:
+                    continue
+                k, h = r["k"], r["h"]
+                assert k.sum() == math.floor(rr * L * n + 0.5)
+                assert np.all(np.diff(k[:h].astype(np.int64)) <= 0)  # non-increasing
+                assert np.all(k[h:] == 0)
+                assert k.max() <= r["n_surv"] <= n
+
+
+def test_drop_all_fuses_every_non_kept_token(orc):
+    # drop_all: the survivor count is n, whatever q, and the kept budgets are
+    # those of the default reading.
+    for L, n, rr in [(28, 3136, 0.28), (4, 512, 0.25), (28, 12544, 0.19)]:
+        a = orc.budget(L=L, n=n, rr=rr)
+        b = orc.budget(L=L, n=n, rr=rr, drop_all=True)
+        assert b["n_surv"] == n and a["n_surv"] < n
+        assert np.array_equal(a["k"], b["k"])

@@ -190,3 +190,17 @@ def test_unit_keep_all_returns_cache(orc):
     np.testing.assert_array_equal(got["kept"], np.arange(40))
     np.testing.assert_array_equal(got["K_out"], K)
     np.testing.assert_array_equal(got["V_out"], _f(V))
+
+
+def test_select_with_every_token_surviving_drops_the_complement(orc):
+    # The fuse-all reading (n_surv = n): the dropped set is exactly the tokens
+    # outside the kept set, in ascending order.
+    rng = np.random.default_rng(11)
+    for n, k in [(64, 10), (300, 1), (300, 299), (5, 0)]:
+        s = rng.random(n).astype(np.float32)
+        kept, drop = orc.select(s, k, n)
+        assert len(kept) == k and len(drop) == n - k
+        assert np.array_equal(np.sort(np.concatenate([kept, drop])), np.arange(n))
+        assert np.all(np.diff(drop) > 0)
+        top = np.argsort(-s.astype(np.float64), kind="stable")[:k]
+        assert set(kept.tolist()) == set(top.tolist())
