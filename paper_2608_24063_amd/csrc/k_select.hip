@@ -4,9 +4,13 @@
 // n_surv - k are dropped (their values get fused), the rest are discarded.
 //
 // One workgroup per unit (256 to 1024 threads, by the longest sequence); each
-// thread holds a contiguous run of up to PER scores in registers.  Scores are non-negative fp32, so their bit
-// patterns order like the values.  The k-th and n_surv-th largest bit patterns
-// are found exactly by a 31-round bisection (both cuts together), ties at a
+// thread holds a contiguous run of up to PER scores in registers.  Scores are
+// non-negative fp32, so their bit patterns order like the values.  The k-th
+// and n_surv-th largest bit patterns are found exactly by a most-significant-
+// digit radix select over the 31 value bits (digits of 8, 8, 8 and 7 bits,
+// both cuts in the same passes): each wave counts the digits of the keys that
+// still match a cut's prefix into its own LDS histogram, and two waves scan
+// the summed histograms for the bin holding the wanted rank.  Ties at a
 // threshold go to the lowest indices, and block-wide prefix sums (DPP wave
 // scans) compact kept and dropped indices in ascending token order.
 #include "vc_device.h"
@@ -15,7 +19,6 @@
 namespace vc {
 
 namespace {
-
 
 // Exclusive prefix over the block of four counters per thread, plus totals.
 template <int kWaves>
@@ -44,18 +47,87 @@ __device__ __forceinline__ void block_scan4(const uint32_t v[4], uint32_t excl[4
   __syncthreads();
 }
 
-__device__ __forceinline__ uint32_t count_wave(bool pred) {
-  return (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(pred));
+// One radix pass for both cuts: digits of `wd` bits at bit `sh`.  On entry
+// pre[c] holds the cut's value bits above the digit and rank[c] the wanted
+// rank (1-based, descending) among the keys sharing them; on exit the digit
+// is fixed and the rank is relative to it.  A rank of 0 (nothing wanted)
+// stays 0.
+template <int kWaves, int PER>
+__device__ __forceinline__ void radix_pass(const uint32_t (&key)[PER], int cnt, int sh, int wd, uint32_t (&pre)[2],
+                                           uint32_t (&rank)[2], uint32_t (*hist)[2][256], uint32_t (*res)[2]) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  // This wave's histogram (the previous pass's scans finished before the
+  // barrier that ended it).
+#pragma unroll
+  for (int i = 0; i < 8; ++i) (&hist[w][0][0])[lane + 64 * i] = 0u;
+  __builtin_amdgcn_wave_barrier();
+  const int top = sh + wd;
+  const uint32_t dm = (1u << wd) - 1u;
+  const uint32_t p0 = top >= 31 ? 0u : pre[0] >> top, p1 = top >= 31 ? 0u : pre[1] >> top;
+  // While both cuts share their prefix (always in the first pass), one
+  // histogram serves both.
+  const bool same = p0 == p1;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    if (i < cnt) {
+      const uint32_t hi = top >= 31 ? 0u : key[i] >> top;
+      const uint32_t dg = (key[i] >> sh) & dm;
+      if (hi == p0) atomicAdd(&hist[w][0][dg], 1u);
+      if (!same && hi == p1) atomicAdd(&hist[w][1][dg], 1u);
+    }
+  }
+  __syncthreads();
+  if (w < 2) {
+    // Wave c scans cut c: lane l owns bins 255-4l .. 252-4l (descending).
+    const int c = w, hc = same ? 0 : w;
+    uint32_t b4[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int q = 0; q < kWaves; ++q) {
+      const uint4 h = *reinterpret_cast<const uint4 *>(&hist[q][hc][252 - 4 * lane]);
+      b4[0] += h.w;
+      b4[1] += h.z;
+      b4[2] += h.y;
+      b4[3] += h.x;
+    }
+    const uint32_t tot = (b4[0] + b4[1]) + (b4[2] + b4[3]);
+    const uint32_t incl = wave_incl_scan(tot);
+    const uint32_t excl = incl - tot;
+    const uint32_t r = rank[c];
+    const uint64_t hit = __builtin_amdgcn_ballot_w64(r > 0 && excl < r && r <= incl);
+    if (hit) {
+      const int src = __builtin_ctzll(hit);
+      if (lane == src) {
+        uint32_t cum = excl, dg = 0u, nr = 0u;
+#pragma unroll
+        for (int j = 3; j >= 0; --j) {  // pick the first bin (descending) that reaches the rank
+          const uint32_t j2 = 3 - j;
+          if (cum < r && r <= cum + b4[j2] && nr == 0u) {
+            dg = 255u - 4u * lane - j2;
+            nr = r - cum;
+          }
+          cum += b4[j2];
+        }
+        res[c][0] = dg;
+        res[c][1] = nr;
+      }
+    } else if (lane == 0) {
+      res[c][0] = 0u;
+      res[c][1] = 0u;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    pre[c] |= res[c][0] << sh;
+    rank[c] = res[c][1];
+  }
 }
 
-// One unit: the k-th and n_surv-th largest score bit patterns are found
-// exactly by bisection over the 31 bit positions, both cuts in the same
-// rounds; each wave counts its keys with ballots, and the wave counts meet in
-// LDS once per round.
 template <int kThreads, int PER>
 __global__ __launch_bounds__(kThreads) void k_select(PrunePlan p) {
   constexpr int kWaves = kThreads / 64;
-  __shared__ __attribute__((aligned(16))) uint32_t red[2][2][kWaves];  // [round parity][cut][wave]
+  __shared__ __attribute__((aligned(16))) uint32_t hist[kWaves][2][256];  // per-wave digit counts per cut
+  __shared__ uint32_t res[2][2];                                          // per cut: digit, rank within it
   __shared__ uint32_t wt[4][kWaves];
 
   const int u = blockIdx.x;  // ((l * B) + b) * Hkv + g, l < h
@@ -76,7 +148,7 @@ __global__ __launch_bounds__(kThreads) void k_select(PrunePlan p) {
 
   const float *S = p.mode ? p.gs + toff
                           : p.S + (int64_t)l * p.Ntot * p.Hkv + toff * p.Hkv + (int64_t)g * n;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x;
   const int per = (n + kThreads - 1) / kThreads;  // <= PER
   const int v0 = tid * per;
   const int cnt = max(0, min(per, n - v0));
@@ -84,7 +156,7 @@ __global__ __launch_bounds__(kThreads) void k_select(PrunePlan p) {
   // Bit patterns of non-negative floats order like the values.  A set sign
   // bit (only possible from non-finite inputs) is mapped to the top of the
   // 31-bit range so every count below stays consistent.  Slots past the
-  // thread's run hold 0, which no bisection candidate (>= 1) counts.
+  // thread's run hold 0 and are never counted.
   uint32_t key[PER];
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
@@ -92,34 +164,14 @@ __global__ __launch_bounds__(kThreads) void k_select(PrunePlan p) {
     key[i] = (x & 0x80000000u) ? 0x7FFFFFFFu : x;
   }
 
-  uint32_t pre[2] = {0u, 0u};
-  const uint32_t need[2] = {(uint32_t)k, (uint32_t)nsv};
-#pragma unroll 1
-  for (int bit = 30, it = 0; bit >= 0; --bit, ++it) {
-    const uint32_t ck = pre[0] | (1u << bit), cs = pre[1] | (1u << bit);
-    uint32_t nk = 0, ns = 0;
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      nk += count_wave(key[i] >= ck);
-      ns += count_wave(key[i] >= cs);
-    }
-    if (lane == 0) {
-      red[it & 1][0][w] = nk;
-      red[it & 1][1][w] = ns;
-    }
-    __syncthreads();
-    uint32_t tk = 0, ts = 0;
-#pragma unroll
-    for (int q = 0; q < kWaves; q += 4) {  // kWaves is a multiple of 4
-      const uint4 a = *reinterpret_cast<const uint4 *>(&red[it & 1][0][q]);
-      const uint4 c = *reinterpret_cast<const uint4 *>(&red[it & 1][1][q]);
-      tk += a.x + a.y + a.z + a.w;
-      ts += c.x + c.y + c.z + c.w;
-    }
-    if (tk >= need[0]) pre[0] = ck;
-    if (ts >= need[1]) pre[1] = cs;
-  }
-  const uint32_t tk = k > 0 ? pre[0] : 0xFFFFFFFFu, ts = pre[1];
+  // Thresholds: the k-th and n_surv-th largest bit patterns (none wanted:
+  // above every key).
+  uint32_t pre[2] = {0u, 0u}, rank[2] = {(uint32_t)k, (uint32_t)nsv};
+  radix_pass<kWaves, PER>(key, cnt, 23, 8, pre, rank, hist, res);
+  radix_pass<kWaves, PER>(key, cnt, 15, 8, pre, rank, hist, res);
+  radix_pass<kWaves, PER>(key, cnt, 7, 8, pre, rank, hist, res);
+  radix_pass<kWaves, PER>(key, cnt, 0, 7, pre, rank, hist, res);
+  const uint32_t tk = k > 0 ? pre[0] : 0xFFFFFFFFu, ts = nsv > 0 ? pre[1] : 0xFFFFFFFFu;
 
   // Counts above and at each threshold; ties fill in ascending index order.
   uint32_t c4[4] = {0, 0, 0, 0};
