@@ -50,6 +50,7 @@ def lib():
             L.orc_budget.argtypes = [i32, i32, f64, i32, f64, i32, i32, P_i32, P_i32, P_i32, P_f64, P_f64]
             L.orc_budget.restype = ctypes.c_int
             L.orc_scores_unit.argtypes = [i32, i32, i32, vp, vp, vp]
+            L.orc_scores_unit_prefill.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp]
             L.orc_select.argtypes = [i32, vp, i32, i32, vp, vp]
             L.orc_gather.argtypes = [i32, i32, vp, vp, vp]
             L.orc_fuse.argtypes = [i32, i32, i32, vp, vp, vp, f64, f64, vp]
@@ -87,6 +88,22 @@ def scores_unit(K: np.ndarray, Q: np.ndarray) -> np.ndarray:
     S = np.zeros(K.shape[0], dtype=np.float64)
     lib().orc_scores_unit(K.shape[0], K.shape[1], Q.shape[0], _p(K), _p(Q), _p(S))
     return S
+
+
+def scores_unit_prefill(K: np.ndarray, Kt: np.ndarray, Q: np.ndarray, with_text: bool = False):
+    """Prefill scoring of one unit.  K: uint16 bf16 bits [n, d] (visual keys);
+    Kt: uint16 [T, d] (text keys); Q: float32 [G, n + T, d] (every token's
+    query, visual tokens first).  Returns fp64 S[n], or (S, St[T]) with
+    with_text."""
+    K = np.ascontiguousarray(K, dtype=np.uint16)
+    d = K.shape[1]
+    Kt = np.ascontiguousarray(Kt, dtype=np.uint16).reshape(-1, d)
+    n, T = K.shape[0], Kt.shape[0]
+    Q = np.ascontiguousarray(Q, dtype=np.float32).reshape(-1, n + T, d)
+    S = np.zeros(max(n, 1), dtype=np.float64)
+    St = np.zeros(max(T, 1), dtype=np.float64)
+    lib().orc_scores_unit_prefill(n, T, d, Q.shape[0], _p(K), _p(Kt) if T else None, _p(Q), _p(S), _p(St))
+    return (S[:n], St[:T]) if with_text else S[:n]
 
 
 def select(score: np.ndarray, k: int, n_surv: int):

@@ -180,6 +180,52 @@ void orc_scores_unit(int32_t n, int32_t d, int32_t rows, const uint16_t *K, cons
 }
 
 /* ------------------------------------------------------------------------ */
+/* Scores: Eq. (token_score) with every prefill token as a query.            */
+/* ------------------------------------------------------------------------ */
+
+void orc_scores_unit_prefill(int32_t n, int32_t T, int32_t d, int32_t G, const uint16_t *K,
+                             const uint16_t *Kt, const float *Q, double *S, double *St) {
+  const int32_t N = n + T;
+  double *qd = (double *)malloc(sizeof(double) * (size_t)d);
+  double *z = (double *)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1));
+  double inv_sqrt_d = 1.0 / sqrt((double)d);
+  for (int32_t v = 0; v < n; ++v) S[v] = 0.0;
+  if (St)
+    for (int32_t t = 0; t < T; ++t) St[t] = 0.0;
+  for (int32_t hh = 0; hh < G; ++hh) {
+    for (int32_t i = 0; i < N; ++i) {
+      /* Token i of the sequence H = concat[H_v, H_q] (visual tokens first);
+       * its query enters the contraction in bf16. */
+      const float *qi = Q + ((int64_t)hh * N + i) * d;
+      for (int32_t j = 0; j < d; ++j) qd[j] = bf(to_bf16(qi[j]));
+      /* Causal self-attention: token i attends tokens 0..i. */
+      double zmax = -INFINITY;
+      for (int32_t j = 0; j <= i; ++j) {
+        const uint16_t *kj = j < n ? K + (int64_t)j * d : Kt + (int64_t)(j - n) * d;
+        double acc = 0.0;
+        for (int32_t x = 0; x < d; ++x) acc += qd[x] * bf(kj[x]);
+        z[j] = acc * inv_sqrt_d;
+        if (z[j] > zmax) zmax = z[j];
+      }
+      double sum = 0.0;
+      for (int32_t j = 0; j <= i; ++j) {
+        z[j] = exp(z[j] - zmax);
+        sum += z[j];
+      }
+      /* A^l_{i,j}; the visual columns accumulate into the score. */
+      for (int32_t j = 0; j <= i; ++j) {
+        if (j < n)
+          S[j] += z[j] / sum;
+        else if (St)
+          St[j - n] += z[j] / sum;
+      }
+    }
+  }
+  free(qd);
+  free(z);
+}
+
+/* ------------------------------------------------------------------------ */
 /* Selection: top-q survivors and top-b_l keep set share one ranking.        */
 /* ------------------------------------------------------------------------ */
 

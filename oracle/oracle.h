@@ -39,6 +39,20 @@ int orc_budget(int32_t L, int32_t n, double rr, int32_t h_param, double m, int32
 void orc_scores_unit(int32_t n, int32_t d, int32_t rows, const uint16_t *K, const float *Q,
                      double *S);
 
+/* Prefill score of one (sequence, layer, kv head) unit, Eq. (token_score)
+ * with every token of the prefill as a query (N = n + T, the sum over
+ * i = 1..N): the sequence is the n visual tokens followed by the T text tokens
+ * (H = concat[H_v, H_q]); query i of each of the G query heads of the group
+ * attends keys 0..i (causal self-attention), visual keys K[j] for j < n and
+ * text keys Kt[j - n]; A_{i,j} = softmax over those keys of
+ * (bf16(q_i) . k_j) / sqrt(d).  S[v] = sum over heads and queries of A_{i,v}
+ * for the visual keys; St[t] (may be NULL) the same for the text keys, so
+ * that sum(S) + sum(St) = G*N.
+ * K: bf16 [n][d]; Kt: bf16 [T][d]; Q: fp32 [G][N][d] (rounded to bf16 first).
+ * S: fp64 [n]; St: fp64 [T]. */
+void orc_scores_unit_prefill(int32_t n, int32_t T, int32_t d, int32_t G, const uint16_t *K,
+                             const uint16_t *Kt, const float *Q, double *S, double *St);
+
 /* Keep / drop partition (Alg. 1 Step 1 and Step 3): order tokens by
  * (score descending, index ascending); kept = the first k, drop = the next
  * n_surv - k; the rest are discarded.  Both lists are written ascending. */

@@ -98,3 +98,84 @@ def test_global_ranking_sum(orc):
     assert s.dtype == np.float32
     assert float(s.astype(np.float64).sum()) == pytest.approx(20.0, rel=1e-6)
     np.testing.assert_array_equal(s, np.sum(units, axis=0).astype(np.float32))
+
+
+# --- Prefill scoring: Eq. (token_score) with every prefill token as a query -----
+# The sequence is n visual tokens then T text tokens; query i attends keys
+# 0..i (causal); the score sums A_{i,v} over heads and queries.
+
+def _prefill_inputs(rng, n, T, d, G, scale=1.5):
+    K = _rand(rng, (n, d), scale)
+    Kt = _rand(rng, (T, d), scale)
+    Q = _f(_rand(rng, (G, n + T, d), scale)).astype(np.float32)
+    return K, Kt, Q
+
+
+@pytest.mark.parametrize("n,T,d,G", [(1, 0, 64, 1), (7, 3, 64, 2), (40, 9, 128, 3), (64, 16, 64, 4)])
+def test_prefill_rows_are_distributions(orc, n, T, d, G):
+    # Every query's causal softmax sums to one: visual plus text columns hold
+    # the G*(n+T) rows' whole mass.
+    rng = np.random.default_rng(n + 31 * T + d + G)
+    K, Kt, Q = _prefill_inputs(rng, n, T, d, G)
+    S, St = orc.scores_unit_prefill(K, Kt, Q, with_text=True)
+    assert S.sum() + St.sum() == pytest.approx(G * (n + T), rel=1e-12)
+    assert np.all(S > 0)
+
+
+@pytest.mark.parametrize("n,T,G", [(1, 0, 1), (5, 0, 2), (12, 4, 3), (33, 7, 2)])
+def test_prefill_identical_keys_harmonic(orc, n, T, G):
+    # All keys equal: query i spreads weight 1/(i+1) over its i+1 keys, so
+    # visual key v scores G * (H_{n+T} - H_v), H_k the k-th harmonic number.
+    rng = np.random.default_rng(n * 5 + T)
+    K = np.repeat(_rand(rng, (1, 64)), n, axis=0)
+    Kt = np.repeat(K[:1], T, axis=0)
+    Q = _f(_rand(rng, (G, n + T, 64), 2.0)).astype(np.float32)
+    S = orc.scores_unit_prefill(K, Kt, Q)
+    H = np.concatenate([[0.0], np.cumsum(1.0 / np.arange(1, n + T + 1))])
+    np.testing.assert_allclose(S, G * (H[n + T] - H[:n]), rtol=1e-13)
+
+
+def test_prefill_first_token_sees_only_itself(orc):
+    # One visual token and no text: its only query attends only it.
+    rng = np.random.default_rng(2)
+    K, Kt, Q = _prefill_inputs(rng, 1, 0, 64, 3)
+    assert orc.scores_unit_prefill(K, Kt, Q)[0] == pytest.approx(3.0, rel=1e-15)
+
+
+def test_prefill_visual_queries_ignore_text(orc):
+    # Causality: visual tokens precede the text, so appending text tokens adds
+    # only the text queries' attention; with the text scored alone the two
+    # parts account for the text rows' mass.
+    rng = np.random.default_rng(17)
+    n, T, d, G = 20, 6, 64, 2
+    K, Kt, Q = _prefill_inputs(rng, n, T, d, G)
+    S0 = orc.scores_unit_prefill(K, Kt[:0], np.ascontiguousarray(Q[:, :n]))
+    S, St = orc.scores_unit_prefill(K, Kt, Q, with_text=True)
+    assert np.all(S - S0 >= -1e-12)
+    assert (S - S0).sum() + St.sum() == pytest.approx(G * T, rel=1e-12)
+    # changing a text key changes the visual scores only through text queries
+    Kt2 = Kt.copy()
+    Kt2[-1] = _rand(rng, (1, d), 3.0)[0]
+    S2 = orc.scores_unit_prefill(K, Kt2, Q)
+    assert not np.allclose(S, S2)
+    Q3 = Q.copy()
+    Q3[:, n:] = 0.0  # text queries with zero logits: uniform over their keys
+    S3 = orc.scores_unit_prefill(K, Kt, Q3)
+    uniform = G * sum(1.0 / (i + 1) for i in range(n, n + T))
+    np.testing.assert_allclose(S3 - S0, uniform, rtol=1e-12)
+
+
+@pytest.mark.parametrize("n,T,d,G", [(9, 4, 64, 2), (16, 0, 128, 1), (5, 11, 64, 3)])
+def test_prefill_brute_force_small(orc, n, T, d, G):
+    # Library softmax of the causally masked logit matrix on tiny units.
+    rng = np.random.default_rng(100 + n + T + d + G)
+    K, Kt, Q = _prefill_inputs(rng, n, T, d, G)
+    keys = np.concatenate([_f(K), _f(Kt).reshape(-1, d)], axis=0)
+    N = n + T
+    ref = np.zeros(n)
+    for h in range(G):
+        q = _f(_bf16(Q[h]))
+        logits = (q @ keys.T) / np.sqrt(d)
+        logits[np.triu_indices(N, 1)] = -np.inf
+        ref += softmax(logits, axis=1)[:, :n].sum(axis=0)
+    np.testing.assert_allclose(orc.scores_unit_prefill(K, Kt, Q), ref, rtol=1e-12)
