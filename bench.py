@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--schedule", default="parabolic", choices=["parabolic", "fixed", "arithmetic", "geometric"],
                     help="layer budget schedule (the budget ablation's alternatives to the parabola)")
     ap.add_argument("--drop-all", action="store_true", help="fuse every non-kept token (n_surv = n)")
+    ap.add_argument("--score-queries", default="window", choices=["window", "prefill"],
+                    help="window: the W trailing text queries score the visual keys; prefill: every "
+                         "prefill token does, causally")
     ap.add_argument("--decode-steps", type=int, default=None)
     ap.add_argument("--no-flush", action="store_true", help="keep caches warm between steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -57,18 +60,29 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic(w, pc, n_list):
+def algorithmic(w, pc, n_list, prefill=False):
     """Per-launch algorithmic work of each stage (bytes, MFMA flops, exps)."""
     L, Hq, Hkv, d, W, G = w.L, w.Hq, w.Hkv, w.d, w.W, w.G
     R = G * W
     Ls = pc.h if pc.params.rank_mode == 0 else L
     out = {}
     k_bytes = sum(Hkv * n * d * 2 for n in n_list) * Ls
-    q_bytes = w.B * Hq * W * d * 4 * Ls
-    flops = sum(Hkv * 2 * R * n * d for n in n_list) * Ls
-    exps = sum(Hkv * R * n for n in n_list) * Ls
-    out["score_stats"] = dict(bytes=k_bytes + q_bytes, flops=flops, exps=exps)
-    out["score_colsum"] = dict(bytes=k_bytes + q_bytes // 2, flops=flops, exps=exps)
+    if not prefill:
+        q_bytes = w.B * Hq * W * d * 4 * Ls
+        flops = sum(Hkv * 2 * R * n * d for n in n_list) * Ls
+        exps = sum(Hkv * R * n for n in n_list) * Ls
+        out["score_stats"] = dict(bytes=k_bytes + q_bytes, flops=flops, exps=exps)
+        out["score_colsum"] = dict(bytes=k_bytes + q_bytes // 2, flops=flops, exps=exps)
+    else:
+        # Every token queries its causal prefix: N(N+1)/2 (query, key) pairs
+        # per head for the row statistics, and n(n+1)/2 + W n pairs that reach
+        # a visual key for the column sums.  Queries are fp32, read once per pass.
+        q_bytes = sum(Hq * (n + W) * d * 4 for n in n_list) * Ls
+        t_bytes = w.B * Hkv * W * d * 2 * Ls
+        p_all = sum(Hkv * G * (n + W) * (n + W + 1) // 2 for n in n_list) * Ls
+        p_vis = sum(Hkv * G * (n * (n + 1) // 2 + W * n) for n in n_list) * Ls
+        out["score_stats"] = dict(bytes=k_bytes + t_bytes + q_bytes, flops=2 * d * p_all, exps=p_all)
+        out["score_colsum"] = dict(bytes=k_bytes + q_bytes, flops=2 * d * p_vis, exps=p_vis)
     fb, ff, fe = 0, 0, 0
     for b, n in enumerate(n_list):
         for l in range(pc.h):
@@ -92,6 +106,8 @@ STAGE_KERNEL = {
     "select": ("k_select", ["k_select.hip"]),
     "gather_fuse": ("k_fuse", ["k_fuse.hip"]),
 }
+PREFILL_STAGE_KERNEL = dict(STAGE_KERNEL, score_stats=("k_pscore_stats", ["k_pscore.hip"]),
+                            score_colsum=("k_pscore_colsum", ["k_pscore.hip"]))
 COPY_PROBE_BYTES = 1 << 30
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_vllm7b_hbm_counters.md")
 
@@ -170,16 +186,17 @@ def reduce_pmc(fetch_dir, write_dir, command):
     print("\n".join(lines))
 
 
-def stored_traffic(stage):
+def stored_traffic(stage, kernels=STAGE_KERNEL):
     """Scaled HBM bytes per dispatch of a stage's kernel, if the stored counters
-    were taken on the current source; else None."""
+    were taken on that kernel's current source; else None."""
     try:
         text = open(TRAFFIC_FILE).read()
         blob = text.split("```json", 1)[1].split("```", 1)[0]
         rec = json.loads(blob)["kernels"].get(stage)
     except (OSError, IndexError, ValueError, KeyError):
         return None
-    if not rec or rec.get("source_hash") != kernel_hash(STAGE_KERNEL[stage][1]):
+    kname, files = kernels[stage]
+    if not rec or rec.get("kernel") != kname or rec.get("source_hash") != kernel_hash(files):
         return None
     return rec["hbm_bytes"]
 
@@ -322,9 +339,11 @@ def decode_latency(w, pc, dev, steps, flush_buf, torch, sg):
                 cold=flush_buf is not None)
 
 
-def cpu_baseline(w, pc, host, units_wanted):
+def cpu_baseline(w, pc, host, units_wanted, prefill=False):
     """The oracle on a bounded sample of the same workload: whole units
     (score, select, gather, fuse) of layer/head ranking, one unit per thread."""
+    import numpy as np
+
     import oracle as orc
     threads = min(16, os.cpu_count() or 1)
     L, Hkv = w.L, w.Hkv
@@ -342,8 +361,18 @@ def cpu_baseline(w, pc, host, units_wanted):
         s0 = toff[b] * Hkv + g * n[b]
         K = host["K"][l][s0:s0 + n[b]]
         V = host["V"][l][s0:s0 + n[b]]
-        Q = host["Q"][l][b, g * w.G:(g + 1) * w.G].reshape(-1, w.d)
-        orc.prune_unit(K, V, Q, pc.k[b * L + l], pc.n_surv[b * L + l])
+        k, ns = pc.k[b * L + l], pc.n_surv[b * L + l]
+        if not prefill:
+            Q = host["Q"][l][b, g * w.G:(g + 1) * w.G].reshape(-1, w.d)
+            orc.prune_unit(K, V, Q, k, ns)
+            return 1
+        N = n[b] + w.W
+        r0 = (toff[b] + b * w.W) * w.Hq + g * w.G * N
+        Q = host["Q"][l][r0:r0 + w.G * N].reshape(w.G, N, w.d)
+        S32 = orc.scores_unit_prefill(K, host["KT"][l][b, g], Q).astype(np.float32)
+        kept, drop = orc.select(S32, k, ns)
+        orc.gather(K, kept)
+        orc.fuse(V, kept, drop)
         return 1
 
     t0 = time.perf_counter()
@@ -384,12 +413,15 @@ def main():
     print(f"[bench] generating {w.name}: B={w.B} L={w.L} Hq={w.Hq} Hkv={w.Hkv} d={w.d} W={w.W} n={n[:4]}",
           file=sys.stderr, flush=True)
     keep_host = not args.no_cpu_baseline
-    dv, host = upload_layers(w, range(w.L), dev, keep_host=keep_host)
+    prefill = args.score_queries == "prefill"
+    dv, host = upload_layers(w, range(w.L), dev, keep_host=keep_host, prefill=prefill)
     sched = {"parabolic": vc.VC_SCHED_PARABOLIC, "fixed": vc.VC_SCHED_FIXED,
              "arithmetic": vc.VC_SCHED_ARITHMETIC, "geometric": vc.VC_SCHED_GEOMETRIC}[args.schedule]
-    params = vc.make_params(w.retention, rank_mode=mode, schedule=sched, drop_all=args.drop_all)
+    params = vc.make_params(w.retention, rank_mode=mode, schedule=sched, drop_all=args.drop_all,
+                            score_queries=vc.VC_SCORE_PREFILL if prefill else vc.VC_SCORE_WINDOW)
     pc = PruneCall(w.B, w.L, w.Hq, w.Hkv, w.d, w.W, n, params, [dv["K"][l] for l in range(w.L)],
-                   [dv["V"][l] for l in range(w.L)], [dv["Q"][l] for l in range(w.L)])
+                   [dv["V"][l] for l in range(w.L)], [dv["Q"][l] for l in range(w.L)],
+                   k_text=[dv["KT"][l] for l in range(w.L)] if prefill else None)
     # Flush by reading (not writing) 1 GiB, so the caches hold clean lines and
     # the measured kernels pay no write-back of the flush data.
     # (float32: a sum of int32 would be widened to int64 first, writing 2 GiB.)
@@ -398,7 +430,7 @@ def main():
     tot, stage, wall = time_prune(pc, args.steps, args.warmup, flush, torch)
     ms = sum(tot) / len(tot)
     in_bytes = sum(w.Hkv * x * w.d * 2 * 2 for x in n) * w.L
-    alg = algorithmic(w, pc, n)
+    alg = algorithmic(w, pc, n, prefill)
     stage_us = {STAGES[i]: 1e3 * sum(s[i] for s in stage) / len(stage) for i in range(6)}
     dom = max(("score_stats", "score_colsum", "select", "gather_fuse"), key=lambda s: stage_us[s])
     a = alg[dom]
@@ -410,8 +442,10 @@ def main():
     else:
         roof = dict(bound="hbm", achieved=a["bytes"] / t / 1e9, peak=HBM_PEAK_GBS, unit="GB/s")
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = stored_traffic(dom)
-    roof["kernel"] = dom
+    kernels = PREFILL_STAGE_KERNEL if prefill else STAGE_KERNEL
+    roof["traffic"] = stored_traffic(dom, kernels)
+    roof["kernel"] = kernels[dom][0]
+    roof["stage"] = dom
     roof["kernel_us"] = stage_us[dom]
     roof["hbm_frac"] = fr_hbm
     roof["mfma_frac"] = fr_mfma
@@ -427,7 +461,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         print(f"[bench] CPU oracle ({args.cpu_units or 'all'} units)", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(w, pc, host, args.cpu_units)
+        cpu = cpu_baseline(w, pc, host, args.cpu_units, prefill)
 
     rec = {
         "metric": "PruneKV compress GB/s (% of HBM peak) + decode-attn speedup vs full KV",
@@ -443,6 +477,7 @@ def main():
         "config": {"workload": f"{w.name}: B={w.B} L={w.L} Hq={w.Hq} Hkv={w.Hkv} d={w.d} "
                                f"{w.frames}x{w.tokens_per_frame} visual tokens, W={w.W}, RR={w.retention}",
                    "rank_mode": args.rank_mode, "schedule": args.schedule, "drop_all": args.drop_all,
+                   "score_queries": args.score_queries,
                    "cold_caches": flush is not None,
                    "input_visual_kv_bytes": in_bytes},
         "hbm_frac_path": alg["path_bytes"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,

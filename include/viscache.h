@@ -67,6 +67,19 @@ typedef enum {
   VC_SCHED_GEOMETRIC = 3
 } vc_schedule;
 
+/* Which queries score the visual tokens (Eq. (token_score): the attention a
+ * token receives, summed over queries).
+ *   WINDOW:  the W trailing text queries of the prefill attend the n_b visual
+ *            keys, softmax over those keys only (the observation-window
+ *            reading; the default).
+ *   PREFILL: every token of the prefill is a query, as the equation is
+ *            written (its sum runs over all N tokens): the sequence is the
+ *            n_b visual tokens followed by the W text tokens, token i attends
+ *            tokens 0..i (causal self-attention, visual then text keys), and a
+ *            visual token's score sums its attention weight over all heads of
+ *            the group and all tokens i at or after it. */
+typedef enum { VC_SCORE_WINDOW = 0, VC_SCORE_PREFILL = 1 } vc_score_queries;
+
 /* Method parameters.  Defaults (viscache_default_params) are the paper's fixed
  * hyper-parameters from Sec. 4, Implementation Details: h = 3/4 L, m = 0.75,
  * tau = 1.0, mu = 0.7, the parabolic schedule, fusion of the top-q
@@ -90,13 +103,16 @@ typedef struct {
                          (Algorithm 1, n_surv = min(n, max(round(q n), k_1)));
                          1: every token outside the kept set (n_surv = n),
                          the reading of Eq. (redistribution) alone. */
+  int32_t score_queries; /* vc_score_queries; default VC_SCORE_WINDOW */
 } vc_params;
 
 /* Problem shape.  L layers, Hq query heads, Hkv kv heads (Hq % Hkv == 0;
  * query head hq reads kv head hq / (Hq/Hkv)), head dim d in {64, 128},
- * W window queries per head, B sequences with n_vis[b] visual tokens each.
- * VC_ERR_UNSUPPORTED beyond the kernels' limits: d, (Hq/Hkv)*W > 1024,
- * n_vis[b] > 32768, or 56*L + 12*B + 16 > 30720 (the layer table and the
+ * W window queries per head (with VC_SCORE_PREFILL: W text tokens per
+ * sequence), B sequences with n_vis[b] visual tokens each.
+ * VC_ERR_UNSUPPORTED beyond the kernels' limits: d, (Hq/Hkv)*W > 1024 with
+ * window scores, (Hq/Hkv)*(n_vis[b] + W) > 2^26 with prefill scores,
+ * n_vis[b] > 32768, or 64*L + 12*B + 16 > 30720 (the layer table and the
  * per-sequence offsets must fit the first 30 KB of the launch plan). */
 typedef struct {
   int32_t B, L, Hq, Hkv, d, W;
@@ -146,6 +162,12 @@ vc_status viscache_prune_score_offsets(const vc_shape *shape, const vc_params *p
  *       index (0..n_b-1) of every kept row.  Output row (b, g, j) sits at
  *       rows[l*(B+1)+b] + g*k[b*L+l] + j, rows ascending in token index.
  *       Layers l >= h have no rows; their pointers may be NULL.
+ *   k_text (read with VC_SCORE_PREFILL only; may be NULL otherwise):
+ *       k_text[l] holds the bf16 keys of the W text tokens of layer l,
+ *       [B][Hkv][W][d].  With VC_SCORE_PREFILL, q_win[l] holds the fp32
+ *       queries of every token instead of the window: row (b, hq, i) at
+ *       (qoff_b*Hq + hq*(n_b + W) + i)*d, qoff_b = sum_{b'<b} (n_b' + W),
+ *       tokens i < n_b visual, then the W text tokens.
  *   drop_out: may be NULL.  Otherwise drop_out[l] receives, per (b, g), the
  *       r = n_surv - k token indices whose values were fused (ascending),
  *       at dropped-row offset sum_{b'<b} Hkv*r_{b',l} + g*r_{b,l}.
@@ -158,12 +180,15 @@ typedef struct {
   void *const *v_out;
   int32_t *const *idx_out;
   int32_t *const *drop_out;
+  const void *const *k_text;
 } vc_prune_io;
 
 /* Device, asynchronous.  PruneKV over all layers and sequences (Algorithm 1):
  * window scores (Eq. (token_score), read as the attention of the W window
  * queries, softmax over the n_b visual keys with scale 1/sqrt(d), summed over
- * the Hq/Hkv query heads of each kv head), budgets as viscache_budget, the
+ * the Hq/Hkv query heads of each kv head; or, with VC_SCORE_PREFILL, the
+ * causal attention of every prefill token as described at vc_score_queries),
+ * budgets as viscache_budget, the
  * keep set (top-k_l) and drop set (ranks k_l+1..n_surv) from one ranking
  * ordered by (score descending, token index ascending), key pruning, and
  * value fusion V_new = mu V_k + (1-mu) softmax(V_k V_d^T / tau) V_d

@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(HERE, "libviscache.so")
 VC_OK, VC_ERR_ARG, VC_ERR_SHAPE, VC_ERR_BUDGET, VC_ERR_WORKSPACE, VC_ERR_UNSUPPORTED, VC_ERR_HIP = range(7)
 VC_RANK_LAYER_HEAD, VC_RANK_GLOBAL = 0, 1
 VC_SCHED_PARABOLIC, VC_SCHED_FIXED, VC_SCHED_ARITHMETIC, VC_SCHED_GEOMETRIC = 0, 1, 2, 3
+VC_SCORE_WINDOW, VC_SCORE_PREFILL = 0, 1
 
 P = ctypes.POINTER
 c_i32, c_i64, c_f32, c_f64, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_void_p
@@ -24,7 +25,8 @@ c_i32, c_i64, c_f32, c_f64, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_floa
 
 class vc_params(ctypes.Structure):
     _fields_ = [("retention", c_f64), ("h", c_i32), ("m", c_f64), ("tau", c_f32), ("mu", c_f32),
-                ("rank_mode", c_i32), ("v_out_fp32", c_i32), ("schedule", c_i32), ("drop_all", c_i32)]
+                ("rank_mode", c_i32), ("v_out_fp32", c_i32), ("schedule", c_i32), ("drop_all", c_i32),
+                ("score_queries", c_i32)]
 
 
 class vc_shape(ctypes.Structure):
@@ -34,7 +36,7 @@ class vc_shape(ctypes.Structure):
 
 class vc_prune_io(ctypes.Structure):
     _fields_ = [("k_in", P(c_vp)), ("v_in", P(c_vp)), ("q_win", P(c_vp)), ("k_out", P(c_vp)),
-                ("v_out", P(c_vp)), ("idx_out", P(c_vp)), ("drop_out", P(c_vp))]
+                ("v_out", P(c_vp)), ("idx_out", P(c_vp)), ("drop_out", P(c_vp)), ("k_text", P(c_vp))]
 
 
 class vc_decode_shape(ctypes.Structure):
@@ -104,11 +106,12 @@ def _check(status: int, what: str) -> None:
 
 def make_params(retention: float, h: int = 0, m: float = 0.75, tau: float = 1.0, mu: float = 0.7,
                 rank_mode: int = VC_RANK_LAYER_HEAD, v_out_fp32: bool = False,
-                schedule: int = VC_SCHED_PARABOLIC, drop_all: bool = False) -> vc_params:
+                schedule: int = VC_SCHED_PARABOLIC, drop_all: bool = False,
+                score_queries: int = VC_SCORE_WINDOW) -> vc_params:
     p = vc_params()
     lib().viscache_default_params(ctypes.byref(p), retention)
     p.h, p.m, p.tau, p.mu, p.rank_mode, p.v_out_fp32 = h, m, tau, mu, rank_mode, int(v_out_fp32)
-    p.schedule, p.drop_all = int(schedule), int(drop_all)
+    p.schedule, p.drop_all, p.score_queries = int(schedule), int(drop_all), int(score_queries)
     return p
 
 
@@ -156,27 +159,28 @@ def _ptrs(seq):
 VC_PRUNE_EVENTS = 7
 
 
-def _io(k_in, v_in, q_win, k_out, v_out, idx_out, drop_out):
+def _io(k_in, v_in, q_win, k_out, v_out, idx_out, drop_out, k_text):
     arrs = [_ptrs(x) for x in (k_in, v_in, q_win, k_out, v_out, idx_out)]
-    drop = _ptrs(drop_out) if drop_out is not None else None
+    opt = [_ptrs(x) if x is not None else None for x in (drop_out, k_text)]
     io = vc_prune_io(*[ctypes.cast(a, P(c_vp)) for a in arrs],
-                     ctypes.cast(drop, P(c_vp)) if drop is not None else None)
-    io._keep = (arrs, drop)
+                     *[ctypes.cast(a, P(c_vp)) if a is not None else None for a in opt])
+    io._keep = (arrs, opt)
     return io
 
 
 def viscache_prune(shape: vc_shape, params: vc_params, k_in, v_in, q_win, k_out, v_out, idx_out,
-                   workspace: int, workspace_bytes: int, stream: int, drop_out=None) -> None:
-    """k_in ... idx_out, drop_out: sequences of L device addresses (ints, 0 for none)."""
-    io = _io(k_in, v_in, q_win, k_out, v_out, idx_out, drop_out)
+                   workspace: int, workspace_bytes: int, stream: int, drop_out=None, k_text=None) -> None:
+    """k_in ... idx_out, drop_out, k_text: sequences of L device addresses (ints, 0 for none)."""
+    io = _io(k_in, v_in, q_win, k_out, v_out, idx_out, drop_out, k_text)
     _check(lib().viscache_prune(ctypes.byref(shape), ctypes.byref(params), ctypes.byref(io),
                                 workspace, workspace_bytes, stream), "viscache_prune")
 
 
 def viscache_prune_staged(shape: vc_shape, params: vc_params, k_in, v_in, q_win, k_out, v_out, idx_out,
-                          workspace: int, workspace_bytes: int, stream: int, events, drop_out=None) -> None:
+                          workspace: int, workspace_bytes: int, stream: int, events, drop_out=None,
+                          k_text=None) -> None:
     """As viscache_prune; `events` = VC_PRUNE_EVENTS raw hipEvent_t handles (ints)."""
-    io = _io(k_in, v_in, q_win, k_out, v_out, idx_out, drop_out)
+    io = _io(k_in, v_in, q_win, k_out, v_out, idx_out, drop_out, k_text)
     ev = (c_vp * VC_PRUNE_EVENTS)(*[int(e) for e in events])
     _check(lib().viscache_prune_staged(ctypes.byref(shape), ctypes.byref(params), ctypes.byref(io),
                                        workspace, workspace_bytes, stream, ev), "viscache_prune_staged")

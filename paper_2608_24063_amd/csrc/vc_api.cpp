@@ -23,6 +23,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 struct Layout {
   int32_t B, L, Hq, Hkv, d, W, G, R, h, Ls, mode, vfp32;
   int32_t nqg, nks, ncol, nfuse, nmax;
+  int32_t prefill, Rmax, nkc;
   int64_t Ntot;
   std::vector<int32_t> n, k, ns;       // n[B], k[B*L], ns[B*L]
   std::vector<int32_t> funit;          // fusion units, longest drop list first
@@ -39,7 +40,6 @@ vc_status check_shape(const vc_shape *s) {
   if (s->B < 1 || s->L < 2 || s->Hq < 1 || s->Hkv < 1 || s->W < 1) return VC_ERR_SHAPE;
   if (s->Hq % s->Hkv != 0) return VC_ERR_SHAPE;
   if (s->d != 64 && s->d != 128) return VC_ERR_UNSUPPORTED;
-  if ((int64_t)(s->Hq / s->Hkv) * s->W > 1024) return VC_ERR_UNSUPPORTED;
   for (int32_t b = 0; b < s->B; ++b)
     if (s->n_vis[b] < 0 || s->n_vis[b] > kMaxTokens) return s->n_vis[b] < 0 ? VC_ERR_SHAPE : VC_ERR_UNSUPPORTED;
   // The layer pointers, token offsets and lengths must fit the plan's first
@@ -61,6 +61,7 @@ vc_status check_params(const vc_params *p, int32_t L) {
   if (p->v_out_fp32 != 0 && p->v_out_fp32 != 1) return VC_ERR_ARG;
   if (p->schedule < VC_SCHED_PARABOLIC || p->schedule > VC_SCHED_GEOMETRIC) return VC_ERR_ARG;
   if (p->drop_all != 0 && p->drop_all != 1) return VC_ERR_ARG;
+  if (p->score_queries != VC_SCORE_WINDOW && p->score_queries != VC_SCORE_PREFILL) return VC_ERR_ARG;
   return VC_OK;
 }
 
@@ -74,6 +75,8 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   y.R = y.G * y.W;
   y.mode = p->rank_mode;
   y.vfp32 = p->v_out_fp32;
+  y.prefill = p->score_queries == VC_SCORE_PREFILL;
+  if (!y.prefill && (int64_t)y.R > 1024) return VC_ERR_UNSUPPORTED;
   y.n.assign(s->n_vis, s->n_vis + s->B);
   y.k.assign((size_t)y.B * y.L, 0);
   y.ns.assign((size_t)y.B * y.L, 0);
@@ -103,7 +106,17 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
     }
   y.nmax = *std::max_element(y.n.begin(), y.n.end());
   const int64_t units = (int64_t)y.Ls * y.B * y.Hkv;
-  y.nqg = (y.R + kStatsRows - 1) / kStatsRows;
+  if (y.prefill) {
+    // Every prefill token queries: a unit has G * (n_b + W) rows.
+    const int64_t rmax = (int64_t)y.G * ((int64_t)y.nmax + y.W);
+    if (rmax > (int64_t(1) << 26)) return VC_ERR_UNSUPPORTED;
+    y.Rmax = (int32_t)std::max<int64_t>(1, rmax);
+    y.nkc = std::max(1, (y.nmax + kPColKeys - 1) / kPColKeys);
+  } else {
+    y.Rmax = y.R;
+    y.nkc = 0;
+  }
+  y.nqg = ((y.prefill ? y.Rmax : y.R) + kStatsRows - 1) / kStatsRows;
   const int64_t base = std::max<int64_t>(1, units * y.nqg);
   // Key splits so that the statistics pass runs in one round of resident
   // workgroups: a second, partial round costs a full workgroup time for a
@@ -111,8 +124,12 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   int64_t nks = std::max<int64_t>(1, kScoreSlots / base);
   nks = std::min<int64_t>(nks, kMaxSplits);
   nks = std::min<int64_t>(nks, std::max(1, (y.nmax + kKeyTile - 1) / kKeyTile));
-  y.nks = (int32_t)std::max<int64_t>(1, nks);
+  y.nks = y.prefill ? 1 : (int32_t)std::max<int64_t>(1, nks);
   y.ncol = std::max(1, (y.nmax + kColKeys - 1) / kColKeys);
+  // A launch holds at most 2^32 - 1 threads: 256-thread workgroups per
+  // (unit, row group, key split) and per (unit, key chunk).
+  if (units * std::max<int64_t>((int64_t)y.nqg * y.nks, std::max(y.nkc, y.ncol)) > (int64_t(1) << 24) - 1)
+    return VC_ERR_UNSUPPORTED;
   y.nfuse = std::max(1, (kmax + kFuseRows - 1) / kFuseRows);
   // Fusion units (layer < h with kept rows), ordered by dropped-row count,
   // descending: every workgroup of a unit walks all of its dropped tiles, so
@@ -195,8 +212,10 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
 
   size_t w = 0;
   y.off_plan = w; w = align_up(w + y.plan_bytes);
-  y.off_qbf = w; w = align_up(w + sizeof(uint16_t) * (size_t)y.Ls * y.B * y.Hq * y.W * y.d);
-  y.off_part = w; w = align_up(w + sizeof(float2) * (size_t)units * y.nks * y.R);
+  y.off_qbf = w;  // bf16 window queries (the prefill passes convert their queries in registers)
+  w = align_up(w + (y.prefill ? 0 : sizeof(uint16_t) * (size_t)y.Ls * y.B * y.Hq * y.W * y.d));
+  y.off_part = w;
+  w = align_up(w + sizeof(float2) * (size_t)units * (y.prefill ? (size_t)y.Rmax : (size_t)y.nks * y.R));
   y.off_S = w; w = align_up(w + sizeof(float) * (size_t)y.Ls * y.Ntot * y.Hkv);
   y.off_gs = w; w = align_up(w + (y.mode == VC_RANK_GLOBAL ? sizeof(float) * (size_t)y.Ntot : 0));
   y.off_drop = w;
@@ -220,6 +239,7 @@ void viscache_default_params(vc_params *p, double retention) {
   p->v_out_fp32 = 0;
   p->schedule = VC_SCHED_PARABOLIC;
   p->drop_all = 0;
+  p->score_queries = VC_SCORE_WINDOW;
 }
 
 vc_status viscache_budget(const vc_shape *shape, const vc_params *params, int32_t *k,
@@ -277,6 +297,11 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return VC_ERR_WORKSPACE;
   for (int32_t l = 0; l < y.Ls; ++l)
     if (y.Ntot > 0 && (!io->k_in[l] || !io->q_win[l])) return VC_ERR_ARG;
+  if (y.prefill && y.W > 0 && y.Ntot > 0) {
+    if (!io->k_text) return VC_ERR_ARG;
+    for (int32_t l = 0; l < y.Ls; ++l)
+      if (!io->k_text[l]) return VC_ERR_ARG;
+  }
   for (int32_t l = 0; l < y.h; ++l) {
     const int64_t rows = y.orow[(size_t)l * (y.B + 1) + y.B];
     if (rows > 0 && (!io->v_in[l] || !io->k_out[l] || !io->v_out[l] || !io->idx_out[l]))
@@ -297,6 +322,7 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
     lp[LP_K_OUT * y.L + l] = l < y.h ? reinterpret_cast<uint64_t>(io->k_out[l]) : 0;
     lp[LP_V_OUT * y.L + l] = l < y.h ? reinterpret_cast<uint64_t>(io->v_out[l]) : 0;
     lp[LP_IDX * y.L + l] = l < y.h ? reinterpret_cast<uint64_t>(io->idx_out[l]) : 0;
+    lp[LP_K_TEXT * y.L + l] = (y.prefill && io->k_text) ? reinterpret_cast<uint64_t>(io->k_text[l]) : 0;
   }
   size_t doff = y.off_drop;
   for (int32_t l = 0; l < y.h; ++l) {
@@ -345,6 +371,7 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   pl.B = y.B; pl.L = y.L; pl.Hq = y.Hq; pl.Hkv = y.Hkv; pl.d = y.d; pl.W = y.W; pl.G = y.G;
   pl.R = y.R; pl.h = y.h; pl.Ls = y.Ls; pl.mode = y.mode; pl.v_fp32 = y.vfp32;
   pl.nqg = y.nqg; pl.nks = y.nks; pl.ncol = y.ncol; pl.nfuse = y.nfuse; pl.nmax = y.nmax;
+  pl.prefill = y.prefill; pl.Rmax = y.Rmax; pl.nkc = y.nkc;
   pl.nfunits = (int32_t)y.funit.size();
   pl.nfwg = (int32_t)y.fwoff.size() - 1;
   pl.sc = (float)(1.4426950408889634 / std::sqrt((double)y.d));
@@ -382,11 +409,12 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   if (blob.size() > first && launch_upload(pb + first, blob.data() + first, blob.size() - first, hs) != hipSuccess)
     return VC_ERR_HIP;
   if (mark(1) != hipSuccess) return VC_ERR_HIP;
-  if (launch_score_stats(pl, reinterpret_cast<uint32_t *>(pb), blob.data(), (uint32_t)(first / 4), hs) !=
+  if ((y.prefill ? launch_pscore_stats(pl, reinterpret_cast<uint32_t *>(pb), blob.data(), (uint32_t)(first / 4), hs)
+                 : launch_score_stats(pl, reinterpret_cast<uint32_t *>(pb), blob.data(), (uint32_t)(first / 4), hs)) !=
       hipSuccess)
     return VC_ERR_HIP;
   if (mark(2) != hipSuccess) return VC_ERR_HIP;
-  if (launch_score_colsum(pl, hs) != hipSuccess) return VC_ERR_HIP;
+  if ((y.prefill ? launch_pscore_colsum(pl, hs) : launch_score_colsum(pl, hs)) != hipSuccess) return VC_ERR_HIP;
   if (mark(3) != hipSuccess) return VC_ERR_HIP;
   if (y.mode == VC_RANK_GLOBAL && launch_score_global(pl, hs) != hipSuccess) return VC_ERR_HIP;
   if (mark(4) != hipSuccess) return VC_ERR_HIP;

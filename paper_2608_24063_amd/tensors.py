@@ -23,10 +23,11 @@ class PruneCall:
     """One PruneKV problem: shape, parameters, per-layer outputs, workspace.
 
     k_in / v_in: per-layer bf16 tensors [sum_b Hkv*n_b, d]; q_win: per-layer
-    fp32 tensors [B, Hq, W, d].  `run()` enqueues viscache_prune on the
-    current stream."""
+    fp32 tensors [B, Hq, W, d] (window scores) or [sum_b Hq*(n_b+W), d]
+    (prefill scores); k_text: per-layer bf16 [B, Hkv, W, d] (prefill scores
+    only).  `run()` enqueues viscache_prune on the current stream."""
 
-    def __init__(self, B, L, Hq, Hkv, d, W, n_vis, params, k_in, v_in, q_win, with_drop=False):
+    def __init__(self, B, L, Hq, Hkv, d, W, n_vis, params, k_in, v_in, q_win, with_drop=False, k_text=None):
         self.B, self.L, self.Hq, self.Hkv, self.d, self.W = B, L, Hq, Hkv, d, W
         self.n_vis = [int(x) for x in n_vis]
         self.params = params
@@ -36,6 +37,7 @@ class PruneCall:
         dev = k_in[0].device
         vdt = torch.float32 if params.v_out_fp32 else torch.bfloat16
         self.k_in, self.v_in, self.q_win = list(k_in), list(v_in), list(q_win)
+        self.k_text = list(k_text) if k_text is not None else None
         self.k_out, self.v_out, self.idx_out, self.drop_out = [], [], [], []
         for l in range(L):
             nrow = self.rows[l * (B + 1) + B]
@@ -64,8 +66,9 @@ class PruneCall:
         objects created with enable_timing=True, or raw hipEvent_t handles as
         ints) the stages are bracketed."""
         drop = [_addr(t) for t in self.drop_out] if self.drop_out else None
+        kt = [_addr(t) for t in self.k_text] if self.k_text is not None else None
         if events is None:
-            viscache_prune(*self._args(), drop_out=drop)
+            viscache_prune(*self._args(), drop_out=drop, k_text=kt)
         else:
             assert len(events) == VC_PRUNE_EVENTS
             handles = []
@@ -76,7 +79,7 @@ class PruneCall:
                 if e.cuda_event == 0:
                     e.record()  # materialise the handle
                 handles.append(e.cuda_event)
-            viscache_prune_staged(*self._args(), handles, drop_out=drop)
+            viscache_prune_staged(*self._args(), handles, drop_out=drop, k_text=kt)
 
     def unit_rows(self, l: int, b: int, g: int):
         """Row range of (layer, sequence, kv head) in layer l's outputs."""

@@ -58,6 +58,8 @@ def lib():
             L.sg_frames_of.restype = ctypes.c_int32
             L.sg_kv_layer.argtypes = [P(_Cfg), ctypes.c_int, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int]
             L.sg_q_layer.argtypes = [P(_Cfg), ctypes.c_int32, ctypes.c_void_p]
+            L.sg_qall_layer.argtypes = [P(_Cfg), ctypes.c_int32, ctypes.c_void_p]
+            L.sg_ktext_layer.argtypes = [P(_Cfg), ctypes.c_int32, ctypes.c_void_p]
             L.sg_normal_bf16.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int64, ctypes.c_void_p]
             L.sg_uniform.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int64, ctypes.c_void_p]
             _lib = L
@@ -141,6 +143,26 @@ class Workload:
         out = np.empty((self.B, self.Hq, self.W, self.d), dtype=np.float32)
         c = self._c()
         lib().sg_q_layer(ctypes.byref(c), layer, out.ctypes.data)
+        return out
+
+    def qall_rows(self) -> int:
+        """Rows of the all-token queries: sum_b Hq * (n_b + W)."""
+        return int((self.n_vis().astype(np.int64) + self.W).sum()) * self.Hq
+
+    def qall_layer(self, layer: int) -> np.ndarray:
+        """fp32 [sum_b Hq*(n_b+W), d]: the query of every prefill token (visual
+        tokens first, then the W text tokens), packed over sequences: row
+        (b, h, i) at qoff_b*Hq + h*(n_b + W) + i, qoff_b = sum_{b'<b} (n_b' + W)."""
+        out = np.empty((self.qall_rows(), self.d), dtype=np.float32)
+        c = self._c()
+        lib().sg_qall_layer(ctypes.byref(c), layer, out.ctypes.data)
+        return out
+
+    def ktext_layer(self, layer: int) -> np.ndarray:
+        """bf16 bits [B, Hkv, W, d]: keys of the W text tokens."""
+        out = np.empty((self.B, self.Hkv, self.W, self.d), dtype=np.uint16)
+        c = self._c()
+        lib().sg_ktext_layer(ctypes.byref(c), layer, out.ctypes.data)
         return out
 
 

@@ -13,22 +13,26 @@ def bf16_tensor(bits: np.ndarray, device) -> torch.Tensor:
     return t.to(device).view(torch.bfloat16)
 
 
-def upload_layers(w: Workload, layers, device, keep_host: bool = False, threads: int | None = None):
-    """Generate K, V (bf16 [rows, d]) and Q (fp32 [B, Hq, W, d]) for `layers`.
+def upload_layers(w: Workload, layers, device, keep_host: bool = False, threads: int | None = None,
+                  prefill: bool = False):
+    """Generate K, V (bf16 [rows, d]) and Q (fp32 [B, Hq, W, d]) for `layers`;
+    with `prefill`, Q is the query of every prefill token (fp32
+    [sum_b Hq*(n_b+W), d]) and 'KT' holds the text keys (bf16 [B, Hkv, W, d]).
 
-    Returns (dev, host): dev maps 'K', 'V', 'Q' to {layer: tensor}; host holds
-    the numpy arrays when keep_host is set (else None)."""
-    dev = {"K": {}, "V": {}, "Q": {}}
-    host = {"K": {}, "V": {}, "Q": {}} if keep_host else None
+    Returns (dev, host): dev maps 'K', 'V', 'Q' (and 'KT') to {layer: tensor};
+    host holds the numpy arrays when keep_host is set (else None)."""
+    roles = ("K", "V", "Q", "KT") if prefill else ("K", "V", "Q")
+    dev = {r: {} for r in roles}
+    host = {r: {} for r in roles} if keep_host else None
     for l in layers:
-        K = w.kv_layer("K", l, threads=threads)
-        V = w.kv_layer("V", l, threads=threads)
-        Q = w.q_layer(l)
-        dev["K"][l] = bf16_tensor(K, device)
-        dev["V"][l] = bf16_tensor(V, device)
-        dev["Q"][l] = torch.from_numpy(Q).to(device)
-        if keep_host:
-            host["K"][l], host["V"][l], host["Q"][l] = K, V, Q
+        arrs = {"K": w.kv_layer("K", l, threads=threads), "V": w.kv_layer("V", l, threads=threads),
+                "Q": w.qall_layer(l) if prefill else w.q_layer(l)}
+        if prefill:
+            arrs["KT"] = w.ktext_layer(l)
+        for r, a in arrs.items():
+            dev[r][l] = torch.from_numpy(a).to(device) if r == "Q" else bf16_tensor(a, device)
+            if keep_host:
+                host[r][l] = a
     return dev, host
 
 

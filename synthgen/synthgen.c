@@ -25,6 +25,10 @@
  *   Window query (b, layer, q head h, row i) = xi + c^K_{b,l,h/G, rel[i mod R]}
  *   with xi ~ N(0, I_d) and rel[] R distinct "relevant" frames per sequence;
  *   stored as fp32 values that are exactly representable in bfloat16.
+ * Prefill scoring (every token of the prefill is a query):
+ *   the query of visual token v = xi + c^K_{b,l,h/G, f(v)} (aligned with its
+ *   own frame); the queries of the W text tokens are the window queries;
+ *   text keys (b, layer, kv head g, token t) ~ N(0, I_d), rounded to bf16.
  */
 #include <math.h>
 #include <pthread.h>
@@ -45,7 +49,7 @@ typedef struct {
 enum {
   ROLE_CENT_K = 1, ROLE_CENT_V = 2, ROLE_NOISE_K = 3, ROLE_NOISE_V = 4,
   ROLE_Q = 5, ROLE_OUTLIER = 6, ROLE_RELEVANT = 7, ROLE_JITTER = 8,
-  ROLE_NORMAL = 9
+  ROLE_NORMAL = 9, ROLE_QVIS = 10, ROLE_KTEXT = 11
 };
 
 static inline uint64_t mix(uint64_t x) {
@@ -245,6 +249,53 @@ int sg_q_layer(const sg_config *c, int32_t layer, float *out) {
       free(cent);
     }
   }
+  return 0;
+}
+
+/* Queries of every prefill token, fp32 (bf16-representable), packed over
+ * sequences: row (b, h, i) at qoff_b*Hq + h*(n_b + W) + i, with
+ * qoff_b = sum_{b' < b} (n_b' + W); i < n_b are the visual tokens, then the
+ * W text tokens (the window queries of sg_q_layer). */
+int sg_qall_layer(const sg_config *c, int32_t layer, float *out) {
+  const int32_t d = c->d, G = c->Hq / c->Hkv;
+  int32_t *n = (int32_t *)malloc(sizeof(int32_t) * c->B);
+  sg_n_vis(c, n);
+  float *win = (float *)malloc(sizeof(float) * (size_t)c->B * c->Hq * c->W * d);
+  sg_q_layer(c, layer, win);
+  int64_t row = 0;
+  for (int32_t b = 0; b < c->B; ++b) {
+    const int32_t F = sg_frames_of(c, b);
+    const int32_t N = n[b] + c->W;
+    for (int32_t h = 0; h < c->Hq; ++h) {
+      float *cent = make_centroids(c, 0, b, layer, h / G, F);
+      uint64_t key = stream_key(c->seed, tensor_id(ROLE_QVIS, (uint64_t)b, (uint64_t)layer, (uint64_t)h));
+      for (int32_t i = 0; i < N; ++i) {
+        float *dst = out + (row + (int64_t)h * N + i) * d;
+        if (i < n[b]) {
+          const float *cf = cent + (int64_t)(i / c->tokens_per_frame) * d;
+          for (int32_t x = 0; x < d; ++x) dst[x] = bf16_round_f32((float)(normal(key, (uint64_t)i * d + x) + (double)cf[x]));
+        } else {
+          memcpy(dst, win + (((int64_t)b * c->Hq + h) * c->W + (i - n[b])) * d, sizeof(float) * (size_t)d);
+        }
+      }
+      free(cent);
+    }
+    row += (int64_t)c->Hq * N;
+  }
+  free(win);
+  free(n);
+  return 0;
+}
+
+/* Keys of the W text tokens, bf16 [B][Hkv][W][d]. */
+int sg_ktext_layer(const sg_config *c, int32_t layer, uint16_t *out) {
+  const int32_t d = c->d;
+  for (int32_t b = 0; b < c->B; ++b)
+    for (int32_t g = 0; g < c->Hkv; ++g) {
+      uint64_t key = stream_key(c->seed, tensor_id(ROLE_KTEXT, (uint64_t)b, (uint64_t)layer, (uint64_t)g));
+      uint16_t *dst = out + (((int64_t)b * c->Hkv + g) * c->W) * d;
+      for (int64_t i = 0; i < (int64_t)c->W * d; ++i) dst[i] = bf16_rne((float)normal(key, (uint64_t)i));
+    }
   return 0;
 }
 

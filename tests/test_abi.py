@@ -177,3 +177,36 @@ def test_decode_row_limit(vc):
     with pytest.raises(vc.VisCacheError) as ei:
         vc.viscache_decode_attn(ds, c, 256, 256, 0.1, 1 << 35, 256, big, 0)
     assert ei.value.status == vc.VC_ERR_UNSUPPORTED
+
+
+def test_prefill_scoring_arguments(vc):
+    """score_queries is validated; prefill scoring lifts the window limit on
+    (Hq/Hkv)*W (its rows are G*(n+W) per unit, up to 2^26), needs no bf16
+    window-query buffer, and needs the text keys of every scored layer."""
+    p = vc.make_params(0.25)
+    assert p.score_queries == vc.VC_SCORE_WINDOW
+    shape = vc.make_shape(1, 4, 8, 2, 64, 32, [512])
+    for bad in (2, -1):
+        q = vc.make_params(0.25, score_queries=bad)
+        with pytest.raises(vc.VisCacheError) as ei:
+            vc.viscache_budget(shape, q)
+        assert ei.value.status == vc.VC_ERR_ARG
+    wide = vc.make_shape(1, 4, 8, 2, 64, 300, [512])
+    assert vc.viscache_prune_workspace_bytes(wide, vc.make_params(0.25)) == 0
+    pre = vc.make_params(0.25, score_queries=vc.VC_SCORE_PREFILL)
+    assert vc.viscache_prune_workspace_bytes(wide, pre) > 0
+    # Window and prefill workspaces differ only in their scratch: the prefill
+    # row statistics (G*(n+W) per unit) replace the window's bf16 queries and
+    # split statistics.
+    assert vc.viscache_prune_workspace_bytes(shape, pre) != vc.viscache_prune_workspace_bytes(shape, p)
+    # Rows beyond 2^26 per unit are refused.
+    huge = vc.make_shape(1, 4, 4096, 1, 64, 16384, [32768])
+    assert vc.viscache_prune_workspace_bytes(huge, pre) == 0
+    need = vc.viscache_prune_workspace_bytes(shape, pre)
+    with pytest.raises(vc.VisCacheError) as ei:  # no text keys
+        vc.viscache_prune(shape, pre, [1] * 4, [1] * 4, [1] * 4, [1] * 4, [1] * 4, [1] * 4, 256, need, 0)
+    assert ei.value.status == vc.VC_ERR_ARG
+    with pytest.raises(vc.VisCacheError) as ei:  # a scored layer without them
+        vc.viscache_prune(shape, pre, [1] * 4, [1] * 4, [1] * 4, [1] * 4, [1] * 4, [1] * 4, 256, need, 0,
+                          k_text=[1, 1, 0, 1])
+    assert ei.value.status == vc.VC_ERR_ARG
