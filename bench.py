@@ -81,8 +81,15 @@ def algorithmic(w, pc, n_list, prefill=False):
         t_bytes = w.B * Hkv * W * d * 2 * Ls
         p_all = sum(Hkv * G * (n + W) * (n + W + 1) // 2 for n in n_list) * Ls
         p_vis = sum(Hkv * G * (n * (n + 1) // 2 + W * n) for n in n_list) * Ls
-        out["score_stats"] = dict(bytes=k_bytes + t_bytes + q_bytes, flops=2 * d * p_all, exps=p_all)
-        out["score_colsum"] = dict(bytes=k_bytes + q_bytes, flops=2 * d * p_vis, exps=p_vis)
+        # One kernel runs both passes (row log-sum-exp, then column sums);
+        # the reduction adds its per-workgroup column partials.
+        out["score_stats"] = dict(bytes=k_bytes + t_bytes + q_bytes, flops=2 * d * (p_all + p_vis),
+                                  exps=p_all + p_vis)
+        units = Ls * w.B * Hkv
+        groups = max(-(-G * (n + W) // 256) for n in n_list)
+        pwg = min(groups, max(1, -(-2048 // units)))
+        out["score_colsum"] = dict(bytes=units * pwg * max(n_list) * 4 + sum(n_list) * Hkv * Ls * 4, flops=0,
+                                   exps=0)
     fb, ff, fe = 0, 0, 0
     for b, n in enumerate(n_list):
         for l in range(pc.h):
@@ -106,8 +113,8 @@ STAGE_KERNEL = {
     "select": ("k_select", ["k_select.hip"]),
     "gather_fuse": ("k_fuse", ["k_fuse.hip"]),
 }
-PREFILL_STAGE_KERNEL = dict(STAGE_KERNEL, score_stats=("k_pscore_stats", ["k_pscore.hip"]),
-                            score_colsum=("k_pscore_colsum", ["k_pscore.hip"]))
+PREFILL_STAGE_KERNEL = dict(STAGE_KERNEL, score_stats=("k_pscore", ["k_pscore.hip"]),
+                            score_colsum=("k_pscore_reduce", ["k_pscore.hip"]))
 COPY_PROBE_BYTES = 1 << 30
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_vllm7b_hbm_counters.md")
 

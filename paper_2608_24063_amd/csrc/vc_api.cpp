@@ -23,7 +23,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 struct Layout {
   int32_t B, L, Hq, Hkv, d, W, G, R, h, Ls, mode, vfp32;
   int32_t nqg, nks, ncol, nfuse, nmax;
-  int32_t prefill, Rmax, nkc;
+  int32_t prefill, pwg;
   int64_t Ntot;
   std::vector<int32_t> n, k, ns;       // n[B], k[B*L], ns[B*L]
   std::vector<int32_t> funit;          // fusion units, longest drop list first
@@ -106,17 +106,19 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
     }
   y.nmax = *std::max_element(y.n.begin(), y.n.end());
   const int64_t units = (int64_t)y.Ls * y.B * y.Hkv;
+  int64_t rows = y.R;  // query rows of the longest unit
+  y.pwg = 0;
   if (y.prefill) {
-    // Every prefill token queries: a unit has G * (n_b + W) rows.
-    const int64_t rmax = (int64_t)y.G * ((int64_t)y.nmax + y.W);
-    if (rmax > (int64_t(1) << 26)) return VC_ERR_UNSUPPORTED;
-    y.Rmax = (int32_t)std::max<int64_t>(1, rmax);
-    y.nkc = std::max(1, (y.nmax + kPColKeys - 1) / kPColKeys);
-  } else {
-    y.Rmax = y.R;
-    y.nkc = 0;
+    // Every prefill token queries: a unit has G * (n_b + W) rows, in groups
+    // of 256.  Enough workgroups per unit for about four rounds of the
+    // resident slots, each owning every pwg-th group of its unit.
+    rows = (int64_t)y.G * ((int64_t)y.nmax + y.W);
+    if (rows > (int64_t(1) << 26)) return VC_ERR_UNSUPPORTED;
+    const int64_t groups = (rows + kStatsRows - 1) / kStatsRows;
+    y.pwg = (int32_t)std::min<int64_t>(
+        groups, std::max<int64_t>(1, (4 * kScoreSlots + units - 1) / std::max<int64_t>(units, 1)));
   }
-  y.nqg = ((y.prefill ? y.Rmax : y.R) + kStatsRows - 1) / kStatsRows;
+  y.nqg = (int32_t)((rows + kStatsRows - 1) / kStatsRows);
   const int64_t base = std::max<int64_t>(1, units * y.nqg);
   // Key splits so that the statistics pass runs in one round of resident
   // workgroups: a second, partial round costs a full workgroup time for a
@@ -127,9 +129,11 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   y.nks = y.prefill ? 1 : (int32_t)std::max<int64_t>(1, nks);
   y.ncol = std::max(1, (y.nmax + kColKeys - 1) / kColKeys);
   // A launch holds at most 2^32 - 1 threads: 256-thread workgroups per
-  // (unit, row group, key split) and per (unit, key chunk).
-  if (units * std::max<int64_t>((int64_t)y.nqg * y.nks, std::max(y.nkc, y.ncol)) > (int64_t(1) << 24) - 1)
-    return VC_ERR_UNSUPPORTED;
+  // (unit, row group, key split) and per (unit, key chunk) for the window
+  // scores; per (unit, share) and per (unit, 256 keys) for the prefill scores.
+  const int64_t per_unit = y.prefill ? std::max<int64_t>(y.pwg, (y.nmax + 255) / 256)
+                                     : std::max<int64_t>((int64_t)y.nqg * y.nks, y.ncol);
+  if (units * per_unit > (int64_t(1) << 24) - 1) return VC_ERR_UNSUPPORTED;
   y.nfuse = std::max(1, (kmax + kFuseRows - 1) / kFuseRows);
   // Fusion units (layer < h with kept rows), ordered by dropped-row count,
   // descending: every workgroup of a unit walks all of its dropped tiles, so
@@ -214,8 +218,9 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   y.off_plan = w; w = align_up(w + y.plan_bytes);
   y.off_qbf = w;  // bf16 window queries (the prefill passes convert their queries in registers)
   w = align_up(w + (y.prefill ? 0 : sizeof(uint16_t) * (size_t)y.Ls * y.B * y.Hq * y.W * y.d));
-  y.off_part = w;
-  w = align_up(w + sizeof(float2) * (size_t)units * (y.prefill ? (size_t)y.Rmax : (size_t)y.nks * y.R));
+  y.off_part = w;  // window row statistics, or the prefill column partials
+  w = align_up(w + (y.prefill ? sizeof(float) * (size_t)units * y.pwg * y.nmax
+                              : sizeof(float2) * (size_t)units * y.nks * y.R));
   y.off_S = w; w = align_up(w + sizeof(float) * (size_t)y.Ls * y.Ntot * y.Hkv);
   y.off_gs = w; w = align_up(w + (y.mode == VC_RANK_GLOBAL ? sizeof(float) * (size_t)y.Ntot : 0));
   y.off_drop = w;
@@ -371,7 +376,7 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   pl.B = y.B; pl.L = y.L; pl.Hq = y.Hq; pl.Hkv = y.Hkv; pl.d = y.d; pl.W = y.W; pl.G = y.G;
   pl.R = y.R; pl.h = y.h; pl.Ls = y.Ls; pl.mode = y.mode; pl.v_fp32 = y.vfp32;
   pl.nqg = y.nqg; pl.nks = y.nks; pl.ncol = y.ncol; pl.nfuse = y.nfuse; pl.nmax = y.nmax;
-  pl.prefill = y.prefill; pl.Rmax = y.Rmax; pl.nkc = y.nkc;
+  pl.prefill = y.prefill; pl.pwg = y.pwg;
   pl.nfunits = (int32_t)y.funit.size();
   pl.nfwg = (int32_t)y.fwoff.size() - 1;
   pl.sc = (float)(1.4426950408889634 / std::sqrt((double)y.d));
@@ -394,6 +399,7 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   pl.fwjob = reinterpret_cast<const int32_t *>(pb + y.p_fwjob);
   pl.qbf = reinterpret_cast<uint16_t *>(ws + y.off_qbf);
   pl.part = reinterpret_cast<float2 *>(ws + y.off_part);
+  pl.pcol = reinterpret_cast<float *>(ws + y.off_part);
   pl.rowst = nullptr;
   pl.cnt = nullptr;
   pl.S = reinterpret_cast<float *>(ws + y.off_S);
@@ -409,12 +415,12 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   if (blob.size() > first && launch_upload(pb + first, blob.data() + first, blob.size() - first, hs) != hipSuccess)
     return VC_ERR_HIP;
   if (mark(1) != hipSuccess) return VC_ERR_HIP;
-  if ((y.prefill ? launch_pscore_stats(pl, reinterpret_cast<uint32_t *>(pb), blob.data(), (uint32_t)(first / 4), hs)
+  if ((y.prefill ? launch_pscore(pl, reinterpret_cast<uint32_t *>(pb), blob.data(), (uint32_t)(first / 4), hs)
                  : launch_score_stats(pl, reinterpret_cast<uint32_t *>(pb), blob.data(), (uint32_t)(first / 4), hs)) !=
       hipSuccess)
     return VC_ERR_HIP;
   if (mark(2) != hipSuccess) return VC_ERR_HIP;
-  if ((y.prefill ? launch_pscore_colsum(pl, hs) : launch_score_colsum(pl, hs)) != hipSuccess) return VC_ERR_HIP;
+  if ((y.prefill ? launch_pscore_reduce(pl, hs) : launch_score_colsum(pl, hs)) != hipSuccess) return VC_ERR_HIP;
   if (mark(3) != hipSuccess) return VC_ERR_HIP;
   if (y.mode == VC_RANK_GLOBAL && launch_score_global(pl, hs) != hipSuccess) return VC_ERR_HIP;
   if (mark(4) != hipSuccess) return VC_ERR_HIP;

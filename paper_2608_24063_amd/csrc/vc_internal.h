@@ -22,7 +22,6 @@ constexpr int kSelectThreads = 1024;
 constexpr int kSelectPerThread = 32;  // => n <= 32768 tokens per sequence
 constexpr int kMaxTokens = kSelectThreads * kSelectPerThread;
 constexpr int kXcdsHost = 8;      // MI355X accelerator dies (host-side grid planning)
-constexpr int kPColKeys = 256;    // visual keys per prefill column-sum workgroup (4 waves x 64)
 
 // One fusion unit (layer, sequence, kv head) with kept rows, as the fusion
 // kernel reads it: absolute addresses of the unit's first rows and its sizes.
@@ -61,8 +60,7 @@ struct PrunePlan {
   int32_t nfwg;       // fusion workgroups (persistent; each walks its job list)
   int32_t nmax;       // max n_b
   int32_t prefill;    // scores from every prefill token (causal) instead of the window
-  int32_t Rmax;       // prefill: most query rows of a unit, G * (n_b + W)
-  int32_t nkc;        // prefill: column-sum key chunks per unit
+  int32_t pwg;        // prefill: workgroups per unit (each owns every pwg-th 256-row group)
   float sc;           // log2(e) / sqrt(d)
   float tc;           // log2(e) / tau
   float mu;
@@ -79,8 +77,8 @@ struct PrunePlan {
   const int32_t *fwoff;  // [nfwg+1] job list offsets per fusion workgroup
   const int32_t *fwjob;  // fusion jobs: unit rank << 8 | 128-row tile
   uint16_t *qbf;        // [Ls][B][Hq][W][d] window queries in bf16
-  float2 *part;         // [U][nks][R] partial row statistics (max*sc, sum);
-                        // prefill: [U][Rmax] final row statistics
+  float2 *part;         // [U][nks][R] partial row statistics (max*sc, sum)
+  float *pcol;          // prefill: [U][pwg][nmax] column partials of each workgroup
   float2 *rowst;        // [U][R] row statistics (max*sc, 1/sum)
   uint32_t *cnt;        // [U] arrival counters of the stats kernel
   float *S;             // [Ls][Ntot*Hkv] window scores
@@ -95,11 +93,11 @@ hipError_t launch_score_stats(const PrunePlan &p, uint32_t *dst, const uint8_t *
                               hipStream_t st);
 hipError_t launch_score_colsum(const PrunePlan &p, hipStream_t st);
 hipError_t launch_score_global(const PrunePlan &p, hipStream_t st);
-// Prefill scores (every prefill token a query, causal); the statistics launch
-// carries the plan's first chunk like launch_score_stats.
-hipError_t launch_pscore_stats(const PrunePlan &p, uint32_t *dst, const uint8_t *src, uint32_t words,
-                               hipStream_t st);
-hipError_t launch_pscore_colsum(const PrunePlan &p, hipStream_t st);
+// Prefill scores (every prefill token a query, causal): column partials per
+// workgroup, carrying the plan's first chunk like launch_score_stats, then
+// their fixed-order sum into S.
+hipError_t launch_pscore(const PrunePlan &p, uint32_t *dst, const uint8_t *src, uint32_t words, hipStream_t st);
+hipError_t launch_pscore_reduce(const PrunePlan &p, hipStream_t st);
 hipError_t launch_select(const PrunePlan &p, hipStream_t st);
 hipError_t launch_fuse(const PrunePlan &p, hipStream_t st);
 
