@@ -139,9 +139,16 @@ def copy_probe(torch, dev):
     del src, dst
 
 
+# Source file of each library kernel (for the hash that dates stored counters).
+KERNEL_SOURCES = {k: files for k, files in list(STAGE_KERNEL.values()) + list(PREFILL_STAGE_KERNEL.values())}
+KERNEL_SOURCES.update({"k_score_global": ["k_score.hip"], "k_upload": ["k_setup.hip"]})
+
+
 def reduce_pmc(fetch_dir, write_dir, command):
-    """Per-dispatch HBM bytes of each prune kernel from two counter runs,
-    scaled by what the same counters read for the copy probe."""
+    """Per-dispatch HBM bytes of each library kernel from two counter runs,
+    scaled by what the same counters read for the copy probe of that run.
+    Records are kept per kernel name and merged into the stored summary, so
+    runs of different configurations (window and prefill scores) add up."""
     import csv
     import glob
     import re
@@ -168,25 +175,34 @@ def reduce_pmc(fetch_dir, write_dir, command):
     if fc <= 0 or wc <= 0:
         raise SystemExit("no copy-probe dispatch found in the counter runs (run bench.py --copy-probe)")
     sf, sw = COPY_PROBE_BYTES / (fc * 1024.0), COPY_PROBE_BYTES / (wc * 1024.0)
-    rec = {"copy_probe_bytes": COPY_PROBE_BYTES, "fetch_kib_copy": fc, "write_kib_copy": wc,
-           "fetch_scale": sf, "write_scale": sw, "kernels": {}}
-    for stage, (kname, files) in STAGE_KERNEL.items():
+    old = {}
+    try:
+        text = open(TRAFFIC_FILE).read()
+        old = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
+    except (OSError, IndexError, ValueError):
+        pass
+    rec = {"copy_probe_bytes": COPY_PROBE_BYTES, "kernels": dict(old.get("kernels", {}))}
+    for kname, files in KERNEL_SOURCES.items():
         if kname not in fetch or kname not in write:
             continue
         fk = sum(v for v, _ in fetch[kname]) / len(fetch[kname])
         wk = sum(v for v, _ in write[kname]) / len(write[kname])
-        rec["kernels"][stage] = {"kernel": kname, "fetch_kib": fk, "write_kib": wk,
+        rec["kernels"][kname] = {"fetch_kib": fk, "write_kib": wk, "fetch_scale": sf, "write_scale": sw,
                                  "hbm_bytes": fk * 1024.0 * sf + wk * 1024.0 * sw,
-                                 "source_hash": kernel_hash(files)}
+                                 "source_hash": kernel_hash(files), "command": command or "(not recorded)"}
     lines = ["# HBM traffic per dispatch, 7B-shaped workload (rocprofv3 FETCH_SIZE / WRITE_SIZE)", "",
-             "Command (each counter in its own run):", "", "```", command or "(not recorded)", "```", "",
-             f"Copy probe: {COPY_PROBE_BYTES} bytes read and written; FETCH_SIZE read {fc:.0f} KiB "
-             f"(scale {sf:.4f}), WRITE_SIZE read {wc:.0f} KiB (scale {sw:.4f}).", "",
-             "| stage | kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled HBM MB |", "|---|---|---|---|---|"]
-    for stage, k in rec["kernels"].items():
-        lines.append(f"| {stage} | {k['kernel']} | {k['fetch_kib']:.0f} | {k['write_kib']:.0f} | "
-                     f"{k['hbm_bytes'] / 1e6:.1f} |")
-    lines += ["", "Machine-readable (read by bench.py):", "", "```json", json.dumps(rec), "```", ""]
+             "Each counter is taken in its own run of the command recorded with the kernel; the copy probe",
+             f"of each run ({COPY_PROBE_BYTES} bytes read and written) calibrates both counters of that run.", "",
+             "| kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | fetch scale | write scale | scaled HBM MB | source hash |",
+             "|---|---|---|---|---|---|---|"]
+    for kname, k in sorted(rec["kernels"].items()):
+        lines.append(f"| {kname} | {k['fetch_kib']:.0f} | {k['write_kib']:.0f} | {k['fetch_scale']:.4f} | "
+                     f"{k['write_scale']:.4f} | {k['hbm_bytes'] / 1e6:.1f} | {k['source_hash']} |")
+    lines += ["", "Commands:", ""]
+    for cmd in sorted({k["command"] for k in rec["kernels"].values()}):
+        names = ", ".join(sorted(n for n, k in rec["kernels"].items() if k["command"] == cmd))
+        lines += [f"- {names}:", "", "  ```", "  " + cmd, "  ```", ""]
+    lines += ["Machine-readable (read by bench.py):", "", "```json", json.dumps(rec), "```", ""]
     os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
     with open(TRAFFIC_FILE, "w") as f:
         f.write("\n".join(lines))
@@ -199,11 +215,11 @@ def stored_traffic(stage, kernels=STAGE_KERNEL):
     try:
         text = open(TRAFFIC_FILE).read()
         blob = text.split("```json", 1)[1].split("```", 1)[0]
-        rec = json.loads(blob)["kernels"].get(stage)
+        kname, files = kernels[stage]
+        rec = json.loads(blob)["kernels"].get(kname)
     except (OSError, IndexError, ValueError, KeyError):
         return None
-    kname, files = kernels[stage]
-    if not rec or rec.get("kernel") != kname or rec.get("source_hash") != kernel_hash(files):
+    if not rec or rec.get("source_hash") != kernel_hash(files):
         return None
     return rec["hbm_bytes"]
 
