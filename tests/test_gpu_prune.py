@@ -551,3 +551,56 @@ def test_vllm7b_prefill_sampled(dev, orc, sg):
             assert check_sets(r.gpu_scores(l, 0, g), r.k[l], r.ns[l], kept, drop) == 0
             # causal rows are distributions: the visual mass is at most G(n+W) rows' worth
             assert 0 < r.gpu_scores(l, 0, g).sum() <= w.G * (r.n[0] + w.W) * (1 + 1e-5)
+
+
+# ---------------------------------------------------------------- limits
+def test_max_sizes_window(dev, orc, sg):
+    """The largest unit the window path takes: n = 32768 visual tokens (the
+    selection's register capacity) and G*W = 1024 window rows (the statistics
+    pass's row limit), d = 128; both layers in full against the oracle."""
+    import paper_2608_24063_amd as vc
+    from paper_2608_24063_amd.tensors import PruneCall
+    from synthgen.device import bf16_tensor
+    L, Hq, Hkv, d, W, n = 2, 16, 1, 128, 64, 32768
+    rng = np.random.default_rng(32768)
+    K = [sg.normal_bf16(0x5EED0100, l, (n, d)) for l in range(L)]
+    V = [sg.normal_bf16(0x5EED0101, l, (n, d)) for l in range(L)]
+    Q = [rng.standard_normal((1, Hq, W, d)).astype(np.float32) for _ in range(L)]
+    params = vc.make_params(0.25)
+    pc = PruneCall(1, L, Hq, Hkv, d, W, [n], params, [bf16_tensor(x, dev) for x in K],
+                   [bf16_tensor(x, dev) for x in V], [torch.from_numpy(q).to(dev) for q in Q], with_drop=True)
+    pc.run()
+    torch.cuda.synchronize()
+    assert pc.h == 2 and pc.n_surv[1] > pc.k[1] > 0
+    refs = orc.run_units(lambda l: orc.scores_unit(K[l], Q[l][0].reshape(-1, d)).astype(np.float32), range(L))
+    for l in range(L):
+        a0, a1 = pc.unit_rows(l, 0, 0)
+        d0, d1 = pc.unit_drop_rows(l, 0, 0)
+        kept = pc.idx_out[l][a0:a1].cpu().numpy()
+        drop = pc.drop_out[l][d0:d1].cpu().numpy()
+        check_sets(refs[l], pc.k[l], pc.n_surv[l], kept, drop, what=f"max l={l}")
+        fref = orc.fuse(V[l], kept.astype(np.int32), drop.astype(np.int32))
+        assert fused_error(fref, pc.v_out[l][a0:a1].float().cpu().numpy()) <= TOL_BF16
+
+
+def test_max_sizes_prefill_identical_keys(dev):
+    """Prefill scores at n = 32768 visual tokens (65 664 query rows per unit,
+    257 row groups): with all keys equal the scores have the closed form
+    G (H_N - H_v) at any size, and the kept and dropped sets are prefixes."""
+    L, Hq, Hkv, d, W, n = 2, 2, 1, 64, 64, 32768
+    G, N = Hq // Hkv, n + W
+    rng = np.random.default_rng(7)
+    row = rng.integers(0, 2 ** 14, (1, d), dtype=np.uint16)
+    K = [np.repeat(row, n, 0) for _ in range(L)]
+    Kt = [np.repeat(row, W, 0).reshape(1, 1, W, d) for _ in range(L)]
+    V = [rng.integers(0, 2 ** 14, (n, d), dtype=np.uint16) for _ in range(L)]
+    Q = [rng.standard_normal((Hq * N, d)).astype(np.float32) for _ in range(L)]
+    pc, S = _prefill_direct(dev, [n], L, Hq, Hkv, d, W, K, V, Kt, Q)
+    H = np.concatenate([[0.0], np.cumsum(1.0 / np.arange(1, N + 1))])
+    ref = G * (H[N] - H[:n])
+    for l in range(pc.h):
+        assert rel_err(ref, S[l][:n]) < 1e-4
+        a0, a1 = pc.unit_rows(l, 0, 0)
+        d0, d1 = pc.unit_drop_rows(l, 0, 0)
+        np.testing.assert_array_equal(pc.idx_out[l][a0:a1].cpu().numpy(), np.arange(pc.k[l]))
+        np.testing.assert_array_equal(pc.drop_out[l][d0:d1].cpu().numpy(), np.arange(pc.k[l], pc.n_surv[l]))
