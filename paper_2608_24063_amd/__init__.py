@@ -168,6 +168,25 @@ def _io(k_in, v_in, q_win, k_out, v_out, idx_out, drop_out, k_text):
     return io
 
 
+def make_prune_io(k_in, v_in, q_win, k_out, v_out, idx_out, drop_out=None, k_text=None) -> vc_prune_io:
+    """A vc_prune_io over sequences of L device addresses (ints, 0 for none),
+    keeping its pointer arrays alive; reusable while the buffers stay put."""
+    return _io(k_in, v_in, q_win, k_out, v_out, idx_out, drop_out, k_text)
+
+
+def prune_with_io(shape: vc_shape, params: vc_params, io: vc_prune_io, workspace: int, workspace_bytes: int,
+                  stream: int, events=None) -> None:
+    """viscache_prune (or viscache_prune_staged with `events`, VC_PRUNE_EVENTS
+    raw hipEvent_t handles) on a prebuilt vc_prune_io."""
+    if events is None:
+        _check(lib().viscache_prune(ctypes.byref(shape), ctypes.byref(params), ctypes.byref(io), workspace,
+                                    workspace_bytes, stream), "viscache_prune")
+    else:
+        ev = (c_vp * VC_PRUNE_EVENTS)(*[int(e) for e in events])
+        _check(lib().viscache_prune_staged(ctypes.byref(shape), ctypes.byref(params), ctypes.byref(io), workspace,
+                                           workspace_bytes, stream, ev), "viscache_prune_staged")
+
+
 def viscache_prune(shape: vc_shape, params: vc_params, k_in, v_in, q_win, k_out, v_out, idx_out,
                    workspace: int, workspace_bytes: int, stream: int, drop_out=None, k_text=None) -> None:
     """k_in ... idx_out, drop_out, k_text: sequences of L device addresses (ints, 0 for none)."""

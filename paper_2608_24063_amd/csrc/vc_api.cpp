@@ -159,6 +159,15 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
     constexpr double kJobStart = 4.0;
     struct Job { double cost; int32_t code; };
     std::vector<std::vector<Job>> xj(kXcdsHost);
+    {
+      std::vector<size_t> per(kXcdsHost, 0);
+      for (size_t rk = 0; rk < y.funit.size(); ++rk) {
+        const int32_t u = y.funit[rk];
+        const int32_t l = u / (y.Hkv * y.B), b = (u / y.Hkv) % y.B;
+        per[rk % kXcdsHost] += (size_t)((y.k[(size_t)b * y.L + l] + kFuseRows - 1) / kFuseRows);
+      }
+      for (int32_t x = 0; x < kXcdsHost; ++x) xj[x].reserve(per[x]);
+    }
     int64_t njobs = 0;
     for (size_t rk = 0; rk < y.funit.size(); ++rk) {
       const int32_t u = y.funit[rk];
@@ -174,25 +183,38 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
     const int32_t per_xcd = (int32_t)std::max<int64_t>(
         1, std::min<int64_t>(kFuseSlots / kXcdsHost, (njobs + kXcdsHost - 1) / kXcdsHost));
     const int32_t nwg = per_xcd * kXcdsHost;
-    std::vector<std::vector<int32_t>> lists(nwg);
+    // Job j of XCD x (in placement order) goes to workgroup x + 8*slot[x][j]:
+    // the least loaded slot, the lowest index among equal loads (a binary
+    // heap on (load, slot)).  Then a counting pass lays the lists out in CSR
+    // form, each list in placement order.
+    std::vector<int32_t> wg_of;  // per job, XCD by XCD in placement order
+    wg_of.reserve((size_t)njobs);
+    std::vector<std::pair<double, int32_t>> heap((size_t)per_xcd);
+    auto later = [](const std::pair<double, int32_t> &a, const std::pair<double, int32_t> &c) {
+      return a.first != c.first ? a.first > c.first : a.second > c.second;
+    };
     for (int32_t x = 0; x < kXcdsHost; ++x) {
       auto &jl = xj[x];
-      std::stable_sort(jl.begin(), jl.end(), [](const Job &a, const Job &c) { return a.cost > c.cost; });
-      std::vector<double> load(per_xcd, 0.0);
+      // Units come longest drop list first, so the jobs usually are in order.
+      auto longer = [](const Job &a, const Job &c) { return a.cost > c.cost; };
+      if (!std::is_sorted(jl.begin(), jl.end(), longer)) std::stable_sort(jl.begin(), jl.end(), longer);
+      for (int32_t i = 0; i < per_xcd; ++i) heap[i] = {0.0, i};
       for (const Job &j : jl) {
-        int32_t best = 0;
-        for (int32_t i = 1; i < per_xcd; ++i)
-          if (load[i] < load[best]) best = i;
-        load[best] += j.cost;
-        lists[x + kXcdsHost * best].push_back(j.code);
+        std::pop_heap(heap.begin(), heap.end(), later);
+        auto &top = heap.back();
+        wg_of.push_back(x + kXcdsHost * top.second);
+        top.first += j.cost;
+        std::push_heap(heap.begin(), heap.end(), later);
       }
     }
-    y.fwoff.assign(1, 0);
-    y.fwjob.clear();
-    for (int32_t w = 0; w < nwg; ++w) {
-      y.fwjob.insert(y.fwjob.end(), lists[w].begin(), lists[w].end());
-      y.fwoff.push_back((int32_t)y.fwjob.size());
-    }
+    y.fwoff.assign((size_t)nwg + 1, 0);
+    for (int32_t w : wg_of) ++y.fwoff[(size_t)w + 1];
+    for (int32_t w = 0; w < nwg; ++w) y.fwoff[(size_t)w + 1] += y.fwoff[(size_t)w];
+    y.fwjob.assign((size_t)njobs, 0);
+    std::vector<int32_t> fill(y.fwoff.begin(), y.fwoff.end() - 1);
+    size_t idx = 0;
+    for (int32_t x = 0; x < kXcdsHost; ++x)
+      for (const Job &j : xj[x]) y.fwjob[(size_t)fill[(size_t)wg_of[idx++]]++] = j.code;
   }
 
   // Plan blob.
@@ -229,6 +251,51 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   return VC_OK;
 }
 
+// The last layout of the calling thread, reused while the shape (with its
+// lengths) and the parameters are unchanged: a serving loop that prunes
+// many requests of one shape, or queries sizes before pruning, plans once.
+struct LayoutKey {
+  int32_t B = 0, L = 0, Hq = 0, Hkv = 0, d = 0, W = 0;
+  std::vector<int32_t> n;
+  double retention = 0, m = 0;
+  float tau = 0, mu = 0;
+  int32_t h = 0, rank_mode = 0, v_out_fp32 = 0, schedule = 0, drop_all = 0, score_queries = 0;
+  bool same(const vc_shape *s, const vc_params *p) const {
+    return B == s->B && L == s->L && Hq == s->Hq && Hkv == s->Hkv && d == s->d && W == s->W &&
+           std::equal(n.begin(), n.end(), s->n_vis) && retention == p->retention && m == p->m && tau == p->tau &&
+           mu == p->mu && h == p->h && rank_mode == p->rank_mode && v_out_fp32 == p->v_out_fp32 &&
+           schedule == p->schedule && drop_all == p->drop_all && score_queries == p->score_queries;
+  }
+  void set(const vc_shape *s, const vc_params *p) {
+    B = s->B; L = s->L; Hq = s->Hq; Hkv = s->Hkv; d = s->d; W = s->W;
+    n.assign(s->n_vis, s->n_vis + s->B);
+    retention = p->retention; m = p->m; tau = p->tau; mu = p->mu; h = p->h; rank_mode = p->rank_mode;
+    v_out_fp32 = p->v_out_fp32; schedule = p->schedule; drop_all = p->drop_all; score_queries = p->score_queries;
+  }
+};
+
+struct LayoutCache {
+  bool valid = false;
+  LayoutKey key;
+  Layout y;
+};
+
+// The layout of (shape, params): the cached one when the key matches, else
+// a fresh one (cached when valid).  nullptr with *st set on an error.
+const Layout *get_layout(const vc_shape *s, const vc_params *p, vc_status *st) {
+  thread_local LayoutCache cache;
+  *st = VC_OK;
+  if (s && p && s->n_vis && s->B >= 1 && cache.valid && cache.key.B == s->B && cache.key.same(s, p))
+    return &cache.y;
+  Layout y;
+  *st = make_layout(s, p, y);
+  if (*st != VC_OK) return nullptr;
+  cache.key.set(s, p);
+  cache.y = std::move(y);
+  cache.valid = true;
+  return &cache.y;
+}
+
 }  // namespace
 
 extern "C" {
@@ -250,9 +317,10 @@ void viscache_default_params(vc_params *p, double retention) {
 vc_status viscache_budget(const vc_shape *shape, const vc_params *params, int32_t *k,
                           int32_t *n_surv, int32_t *h_out) {
   if (!k || !n_surv) return VC_ERR_ARG;
-  Layout y;
-  vc_status st = make_layout(shape, params, y);
-  if (st != VC_OK) return st;
+  vc_status st;
+  const Layout *yp = get_layout(shape, params, &st);
+  if (!yp) return st;
+  const Layout &y = *yp;
   std::memcpy(k, y.k.data(), sizeof(int32_t) * y.k.size());
   std::memcpy(n_surv, y.ns.data(), sizeof(int32_t) * y.ns.size());
   if (h_out) *h_out = y.h;
@@ -261,25 +329,27 @@ vc_status viscache_budget(const vc_shape *shape, const vc_params *params, int32_
 
 vc_status viscache_out_rows(const vc_shape *shape, const vc_params *params, int64_t *rows) {
   if (!rows) return VC_ERR_ARG;
-  Layout y;
-  vc_status st = make_layout(shape, params, y);
-  if (st != VC_OK) return st;
+  vc_status st;
+  const Layout *yp = get_layout(shape, params, &st);
+  if (!yp) return st;
+  const Layout &y = *yp;
   std::memcpy(rows, y.orow.data(), sizeof(int64_t) * y.orow.size());
   return VC_OK;
 }
 
 size_t viscache_prune_workspace_bytes(const vc_shape *shape, const vc_params *params) {
-  Layout y;
-  if (make_layout(shape, params, y) != VC_OK) return 0;
-  return y.total;
+  vc_status st;
+  const Layout *yp = get_layout(shape, params, &st);
+  return yp ? yp->total : 0;
 }
 
 vc_status viscache_prune_score_offsets(const vc_shape *shape, const vc_params *params,
                                        size_t *scores_off, size_t *shared_off) {
   if (!scores_off || !shared_off) return VC_ERR_ARG;
-  Layout y;
-  vc_status st = make_layout(shape, params, y);
-  if (st != VC_OK) return st;
+  vc_status st;
+  const Layout *yp = get_layout(shape, params, &st);
+  if (!yp) return st;
+  const Layout &y = *yp;
   *scores_off = y.off_S;
   *shared_off = y.mode == VC_RANK_GLOBAL ? y.off_gs : (size_t)-1;
   return VC_OK;
@@ -293,9 +363,10 @@ vc_status viscache_prune(const vc_shape *shape, const vc_params *params, const v
 vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, const vc_prune_io *io,
                                 void *workspace, size_t workspace_bytes, void *stream,
                                 void *const *events) {
-  Layout y;
-  vc_status st = make_layout(shape, params, y);
-  if (st != VC_OK) return st;
+  vc_status st;
+  const Layout *yp = get_layout(shape, params, &st);
+  if (!yp) return st;
+  const Layout &y = *yp;
   if (!io || !io->k_in || !io->v_in || !io->q_win || !io->k_out || !io->v_out || !io->idx_out)
     return VC_ERR_ARG;
   if (!workspace || workspace_bytes < y.total) return VC_ERR_WORKSPACE;
@@ -400,8 +471,6 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   pl.qbf = reinterpret_cast<uint16_t *>(ws + y.off_qbf);
   pl.part = reinterpret_cast<float2 *>(ws + y.off_part);
   pl.pcol = reinterpret_cast<float *>(ws + y.off_part);
-  pl.rowst = nullptr;
-  pl.cnt = nullptr;
   pl.S = reinterpret_cast<float *>(ws + y.off_S);
   pl.gs = y.mode == VC_RANK_GLOBAL ? reinterpret_cast<float *>(ws + y.off_gs) : nullptr;
 

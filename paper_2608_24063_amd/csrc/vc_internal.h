@@ -79,8 +79,6 @@ struct PrunePlan {
   uint16_t *qbf;        // [Ls][B][Hq][W][d] window queries in bf16
   float2 *part;         // [U][nks][R] partial row statistics (max*sc, sum)
   float *pcol;          // prefill: [U][pwg][nmax] column partials of each workgroup
-  float2 *rowst;        // [U][R] row statistics (max*sc, 1/sum)
-  uint32_t *cnt;        // [U] arrival counters of the stats kernel
   float *S;             // [Ls][Ntot*Hkv] window scores
   float *gs;            // [Ntot] shared (global) scores
 };

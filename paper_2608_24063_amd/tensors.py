@@ -5,10 +5,10 @@ from __future__ import annotations
 
 import torch
 
-from . import (VC_PRUNE_EVENTS, VC_RANK_GLOBAL, make_params, make_shape, vc_cache, vc_decode_shape,
-               viscache_append_kv, viscache_budget, viscache_decode_attn, viscache_decode_step,
-               viscache_decode_step_workspace_bytes, viscache_decode_workspace_bytes,
-               viscache_out_rows, viscache_prune, viscache_prune_staged, viscache_prune_workspace_bytes)
+from . import (VC_PRUNE_EVENTS, VC_RANK_GLOBAL, make_params, make_prune_io, make_shape, prune_with_io, vc_cache,
+               vc_decode_shape, viscache_append_kv, viscache_budget, viscache_decode_attn, viscache_decode_step,
+               viscache_decode_step_workspace_bytes, viscache_decode_workspace_bytes, viscache_out_rows,
+               viscache_prune_workspace_bytes)
 
 
 def _stream() -> int:
@@ -49,27 +49,28 @@ class PruneCall:
                 self.drop_out.append(torch.empty((ndrop,), dtype=torch.int32, device=dev))
         self.ws_bytes = viscache_prune_workspace_bytes(self.shape, params)
         self.ws = torch.empty((self.ws_bytes,), dtype=torch.uint8, device=dev)
+        self._io = None
 
     @property
     def global_rank(self) -> bool:
         return self.params.rank_mode == VC_RANK_GLOBAL
 
-    def _args(self):
-        return (self.shape, self.params,
-                [_addr(t) for t in self.k_in], [_addr(t) for t in self.v_in],
-                [_addr(t) for t in self.q_win], [_addr(t) for t in self.k_out],
-                [_addr(t) for t in self.v_out], [_addr(t) for t in self.idx_out],
-                self.ws.data_ptr(), self.ws_bytes, _stream())
+    def _prune_io(self):
+        """The call's vc_prune_io, built once (the buffers never move)."""
+        if self._io is None:
+            a = lambda ts: [_addr(t) for t in ts]
+            self._io = make_prune_io(a(self.k_in), a(self.v_in), a(self.q_win), a(self.k_out), a(self.v_out),
+                                     a(self.idx_out), a(self.drop_out) if self.drop_out else None,
+                                     a(self.k_text) if self.k_text is not None else None)
+        return self._io
 
     def run(self, events=None) -> None:
-        """Enqueue viscache_prune; with `events` (VC_PRUNE_EVENTS torch.cuda.Event
-        objects created with enable_timing=True, or raw hipEvent_t handles as
-        ints) the stages are bracketed."""
-        drop = [_addr(t) for t in self.drop_out] if self.drop_out else None
-        kt = [_addr(t) for t in self.k_text] if self.k_text is not None else None
-        if events is None:
-            viscache_prune(*self._args(), drop_out=drop, k_text=kt)
-        else:
+        """Enqueue viscache_prune on the current stream; with `events`
+        (VC_PRUNE_EVENTS torch.cuda.Event objects created with
+        enable_timing=True, or raw hipEvent_t handles as ints) the stages are
+        bracketed (viscache_prune_staged)."""
+        handles = None
+        if events is not None:
             assert len(events) == VC_PRUNE_EVENTS
             handles = []
             for e in events:
@@ -79,7 +80,8 @@ class PruneCall:
                 if e.cuda_event == 0:
                     e.record()  # materialise the handle
                 handles.append(e.cuda_event)
-            viscache_prune_staged(*self._args(), handles, drop_out=drop, k_text=kt)
+        prune_with_io(self.shape, self.params, self._prune_io(), self.ws.data_ptr(), self.ws_bytes, _stream(),
+                      handles)
 
     def unit_rows(self, l: int, b: int, g: int):
         """Row range of (layer, sequence, kv head) in layer l's outputs."""

@@ -210,3 +210,29 @@ def test_prefill_scoring_arguments(vc):
         vc.viscache_prune(shape, pre, [1] * 4, [1] * 4, [1] * 4, [1] * 4, [1] * 4, [1] * 4, 256, need, 0,
                           k_text=[1, 1, 0, 1])
     assert ei.value.status == vc.VC_ERR_ARG
+
+
+def test_layout_reuse_follows_contents(vc, orc):
+    """The library reuses its last plan while shape, lengths and parameters
+    are unchanged: results must follow the contents, not the pointers."""
+    import ctypes
+    arr = (ctypes.c_int32 * 2)(3136, 700)
+    shape = vc.vc_shape(2, 28, 28, 4, 128, 64, ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32)))
+    p = vc.make_params(0.28)
+    k1, _, _ = vc.viscache_budget(shape, p)
+    assert k1[:28] == list(orc.budget(L=28, n=3136, rr=0.28)["k"])
+    arr[1] = 1500  # same array, new length
+    k2, _, _ = vc.viscache_budget(shape, p)
+    assert k2[28:] == list(orc.budget(L=28, n=1500, rr=0.28)["k"])
+    assert vc.viscache_out_rows(shape, p)[-1] == 4 * (k2[27] + k2[55])
+    p.retention = 0.19  # same struct, new retention
+    k3, _, _ = vc.viscache_budget(shape, p)
+    assert k3[:28] == list(orc.budget(L=28, n=3136, rr=0.19)["k"])
+    p.tau = 0.0  # an invalid parameter is still refused after a valid call
+    with pytest.raises(vc.VisCacheError) as ei:
+        vc.viscache_budget(shape, p)
+    assert ei.value.status == vc.VC_ERR_ARG
+    p.tau = 1.0
+    assert vc.viscache_budget(shape, p)[0] == k3
+    one = vc.make_shape(1, 28, 28, 4, 128, 64, [3136])  # fewer sequences than the cached plan
+    assert vc.viscache_budget(one, p)[0] == k3[:28]
