@@ -11,7 +11,11 @@
  *     process memory.  Each argument says which one it is.
  *   - The caller owns every buffer.  The library never allocates or frees
  *     device memory, never synchronises a stream and keeps no mutable global
- *     state: calls on different streams with different buffers may overlap.
+ *     state shared between threads: calls on different streams with
+ *     different buffers may overlap.  Each calling thread keeps a host copy
+ *     of its last plan (budgets, offsets, fusion job lists) and reuses it
+ *     while the shape, the lengths n_vis[] and the parameters compare equal
+ *     by value, so repeated calls of one shape plan once.
  *   - Sizes of outputs and of the workspace come from the host-only query
  *     functions below, so the device path needs no device-to-host copy.
  *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
