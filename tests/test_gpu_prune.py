@@ -604,3 +604,31 @@ def test_max_sizes_prefill_identical_keys(dev):
         d0, d1 = pc.unit_drop_rows(l, 0, 0)
         np.testing.assert_array_equal(pc.idx_out[l][a0:a1].cpu().numpy(), np.arange(pc.k[l]))
         np.testing.assert_array_equal(pc.drop_out[l][d0:d1].cpu().numpy(), np.arange(pc.k[l], pc.n_surv[l]))
+
+
+# ---------------------------------------------------------- graph capture
+def test_graph_capture_replays(dev, orc, sg):
+    """A captured viscache_prune replays to the eager result every time, with
+    eager work and overwritten outputs between the replays."""
+    w = _custom(sg, L=8, frame_jitter=0)
+    r = Run(w, dev)
+    pc = r.pc
+    ref = [t.clone() for t in pc.v_out] + [t.clone() for t in pc.idx_out]
+    outs = pc.v_out + pc.idx_out
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            pc.run()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    for rep in range(4):
+        for t in outs:
+            t.fill_(7)
+        x = torch.randn(1 << 20, device=dev).sum()  # eager work between replays
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(ref, outs):
+            assert torch.equal(a, b), f"replay {rep}"
+        del x
