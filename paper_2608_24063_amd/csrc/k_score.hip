@@ -270,8 +270,8 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p, uint32_t *p
 }
 
 // ---------------------------------------------------------------------------
-// Pass 2: column sums.  Workgroup = (unit, 128-key chunk).  Wave w owns keys
-// chunk*128 + w*32 + [0, 32) as B operands; the G*W query rows (bf16 copies
+// Pass 2: column sums.  Workgroup = (unit, 256-key chunk).  Wave w owns keys
+// chunk*256 + w*64 + [0, 64) as B operands; the G*W query rows (bf16 copies
 // written by pass 1) stream through LDS 64 rows at a time as A operands, so the
 // product is Z (queries x keys): lane l sees key l%16 of each 16-key block and
 // rows 4*(l/16)+i, and accumulates exp2(z*sc - m_r) / sum_r per key.
@@ -304,11 +304,11 @@ __global__ __launch_bounds__(256, 3) void k_score_colsum(PrunePlan p) {
                        ((int64_t)b * p.Hq + (int64_t)g * p.G) * p.W * D;
 
   // Keys of this wave as B operands.
-  const int key0 = c * kColKeys + w * 32;
+  const int key0 = c * kColKeys + w * 64;
   const bool active = key0 < n;  // wave-uniform
-  bf16x8 bk[2][KS];
+  bf16x8 bk[4][KS];
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb) {
+  for (int kb = 0; kb < 4; ++kb) {
     const int key = key0 + kb * 16 + lr;
 #pragma unroll
     for (int s = 0; s < KS; ++s)
@@ -344,37 +344,42 @@ __global__ __launch_bounds__(256, 3) void k_score_colsum(PrunePlan p) {
   tr.store(qt[0], tid);
   __syncthreads();
 
-  float col[2] = {0.f, 0.f};
+  float col[4] = {0.f, 0.f, 0.f, 0.f};
   const int ntiles = Rpad / 64;
   for (int t = 0; t < ntiles; ++t) {
     if (t + 1 < ntiles) tr.load(Qb, (t + 1) * 64, R, tid);
     if (active) {
       const uint16_t *ql = qt[t & 1];
-      // Four query blocks x two key blocks: eight accumulation chains.
-      f32x4 acc[4][2];
+      // Two halves of two query blocks x four key blocks: eight accumulation
+      // chains at a time, every operand read from LDS feeding four products.
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        bf16x8 a[4];
+      for (int qh = 0; qh < 2; ++qh) {
+        f32x4 acc[2][4];
 #pragma unroll
-        for (int qb = 0; qb < 4; ++qb)
-          a[qb] = as_bf16x8(*reinterpret_cast<const u32x4 *>(ql + (qb * 16 + lr) * P + 32 * s + 8 * lg));
+        for (int s = 0; s < KS; ++s) {
+          bf16x8 a[2];
 #pragma unroll
-        for (int qb = 0; qb < 4; ++qb)
+          for (int q2 = 0; q2 < 2; ++q2)
+            a[q2] = as_bf16x8(*reinterpret_cast<const u32x4 *>(ql + ((2 * qh + q2) * 16 + lr) * P + 32 * s + 8 * lg));
 #pragma unroll
-          for (int kb = 0; kb < 2; ++kb)
-            acc[qb][kb] = mfma_bf16(a[qb], bk[kb][s], s == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : acc[qb][kb]);
-      }
+          for (int q2 = 0; q2 < 2; ++q2)
 #pragma unroll
-      for (int qb = 0; qb < 4; ++qb) {
-        const int rbase = t * 64 + qb * 16 + 4 * lg;
-        const f32x4 s01 = *reinterpret_cast<const f32x4 *>(&rs[rbase]);
-        const f32x4 s23 = *reinterpret_cast<const f32x4 *>(&rs[rbase + 2]);
-        const float mr[4] = {s01.x, s01.z, s23.x, s23.z}, ir[4] = {s01.y, s01.w, s23.y, s23.w};
+            for (int kb = 0; kb < 4; ++kb)
+              acc[q2][kb] = mfma_bf16(a[q2], bk[kb][s], s == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : acc[q2][kb]);
+        }
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+        for (int q2 = 0; q2 < 2; ++q2) {
+          const int qb = 2 * qh + q2;
+          const int rbase = t * 64 + qb * 16 + 4 * lg;
+          const f32x4 s01 = *reinterpret_cast<const f32x4 *>(&rs[rbase]);
+          const f32x4 s23 = *reinterpret_cast<const f32x4 *>(&rs[rbase + 2]);
+          const float mr[4] = {s01.x, s01.z, s23.x, s23.z}, ir[4] = {s01.y, s01.w, s23.y, s23.w};
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            col[kb] = fmaf(fast_exp2(fmaf(acc[qb][kb][i], sc, -mr[i])), ir[i], col[kb]);
+          for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              col[kb] = fmaf(fast_exp2(fmaf(acc[q2][kb][i], sc, -mr[i])), ir[i], col[kb]);
+        }
       }
     }
     if (t + 1 < ntiles) tr.store(qt[(t + 1) & 1], tid);
@@ -384,7 +389,7 @@ __global__ __launch_bounds__(256, 3) void k_score_colsum(PrunePlan p) {
 
   float *S = p.S + (int64_t)ls * p.Ntot * p.Hkv + toff * p.Hkv + (int64_t)g * n;
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb) {
+  for (int kb = 0; kb < 4; ++kb) {
     float v = col[kb];
     v += shfl_xor(v, 16);
     v += shfl_xor(v, 32);

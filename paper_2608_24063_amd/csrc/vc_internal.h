@@ -13,7 +13,7 @@ enum { LP_K_IN = 0, LP_V_IN, LP_Q, LP_K_OUT, LP_V_OUT, LP_IDX, LP_DROP, LP_K_TEX
 // Tile sizes shared by host-side grid sizing and the kernels.
 constexpr int kStatsRows = 256;   // query rows per stats workgroup (4 waves x 64)
 constexpr int kKeyTile = 64;      // keys staged per LDS tile
-constexpr int kColKeys = 128;     // keys per column-sum workgroup (4 waves x 32)
+constexpr int kColKeys = 256;     // keys per column-sum workgroup (4 waves x 64)
 constexpr int kScoreSlots = 512;  // resident stats workgroups (256 CUs x 2)
 constexpr int kMaxSplits = 8;     // key splits of the stats pass
 constexpr int kFuseRows = 128;    // kept rows per fusion workgroup (4 waves x 32)
