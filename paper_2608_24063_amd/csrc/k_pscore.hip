@@ -212,19 +212,31 @@ __global__ __launch_bounds__(256, 2) void k_pscore(PrunePlan p, uint32_t *plan_d
                 for (int i = 0; i < 4; ++i)
                   if (tb + (2 * kh + k2) * 16 + 4 * lg + i > pos[qb]) acc[k2][i] = kNegInf;
             }
-            float tm = kNegInf;
-#pragma unroll
-            for (int k2 = 0; k2 < 2; ++k2)
-#pragma unroll
-              for (int i = 0; i < 4; ++i) tm = fmaxf(tm, acc[k2][i]);
-            const float mnew = fmaxf(m[qb], tm * sc);
+            // Exponentials against the running max as it stands; only when
+            // they grow past 2^96 (the row's first keys, or a logit far above
+            // the earlier ones) is the max raised and the half redone.
             float part = 0.f;
 #pragma unroll
             for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
-              for (int i = 0; i < 4; ++i) part += fast_exp2(fmaf(acc[k2][i], sc, -mnew));
-            sum[qb] = fmaf(sum[qb], fast_exp2(m[qb] - mnew), part);
-            m[qb] = mnew;
+              for (int i = 0; i < 4; ++i) part += fast_exp2(fmaf(acc[k2][i], sc, -m[qb]));
+            if (part <= 0x1p96f) {
+              sum[qb] += part;
+            } else {
+              float tm = kNegInf;
+#pragma unroll
+              for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) tm = fmaxf(tm, acc[k2][i]);
+              const float mnew = fmaxf(m[qb], tm * sc);
+              part = 0.f;
+#pragma unroll
+              for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) part += fast_exp2(fmaf(acc[k2][i], sc, -mnew));
+              sum[qb] = fmaf(sum[qb], fast_exp2(m[qb] - mnew), part);
+              m[qb] = mnew;
+            }
           }
         }
       }

@@ -86,19 +86,31 @@ __device__ __forceinline__ void stats_rows(f32x4 (&acc)[4], float &m, float &sum
       for (int i = 0; i < 4; ++i)
         if (tb + kb * 16 + 4 * lg + i >= k1) acc[kb][i] = kNegInf;
   }
-  float tm = acc[0][0];
-#pragma unroll
-  for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) tm = fmaxf(tm, acc[kb][i]);
-  const float mnew = fmaxf(m, tm * sc);  // scaled running max
+  // Exponentials against the running max as it stands; only when they grow
+  // past 2^96 (a logit far above every earlier one, or the first tile) is
+  // the max raised and the tile redone.
   float part = 0.f;
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) part += fast_exp2(fmaf(acc[kb][i], sc, -mnew));
-  sum = fmaf(sum, fast_exp2(m - mnew), part);
-  m = mnew;
+    for (int i = 0; i < 4; ++i) part += fast_exp2(fmaf(acc[kb][i], sc, -m));
+  if (part <= 0x1p96f) {
+    sum += part;
+  } else {
+    float tm = acc[0][0];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) tm = fmaxf(tm, acc[kb][i]);
+    const float mnew = fmaxf(m, tm * sc);  // scaled running max
+    part = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) part += fast_exp2(fmaf(acc[kb][i], sc, -mnew));
+    sum = fmaf(sum, fast_exp2(m - mnew), part);
+    m = mnew;
+  }
 }
 
 // One 64-key tile against the wave's four 16-row query blocks.  The K tile's
