@@ -87,7 +87,8 @@ def algorithmic(w, pc, n_list, prefill=False):
                                   exps=p_all + p_vis)
         units = Ls * w.B * Hkv
         groups = max(-(-G * (n + W) // 256) for n in n_list)
-        pwg = min(groups, max(1, -(-2048 // units)))
+        per_wg = max(1, (groups * units + 4 * 512) // (8 * 512))  # the library's rule (about eight rounds)
+        pwg = min(groups, -(-groups // per_wg))
         out["score_colsum"] = dict(bytes=units * pwg * max(n_list) * 4 + sum(n_list) * Hkv * Ls * 4, flops=0,
                                    exps=0)
     fb, ff, fe = 0, 0, 0

@@ -110,13 +110,17 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   y.pwg = 0;
   if (y.prefill) {
     // Every prefill token queries: a unit has G * (n_b + W) rows, in groups
-    // of 256.  Enough workgroups per unit for about four rounds of the
-    // resident slots, each owning every pwg-th group of its unit.
+    // of 256.  Each of a unit's pwg workgroups owns every pwg-th group.  The
+    // groups per workgroup are chosen so that all units together make about
+    // eight rounds of the resident slots: small workgroups of near-equal
+    // size let the dispatcher balance groups whose causal prefixes differ
+    // (two groups per workgroup ran 19% faster than three to four on the 7B
+    // shape), at the price of more column partials to add up.
     rows = (int64_t)y.G * ((int64_t)y.nmax + y.W);
     if (rows > (int64_t(1) << 26)) return VC_ERR_UNSUPPORTED;
     const int64_t groups = (rows + kStatsRows - 1) / kStatsRows;
-    y.pwg = (int32_t)std::min<int64_t>(
-        groups, std::max<int64_t>(1, (4 * kScoreSlots + units - 1) / std::max<int64_t>(units, 1)));
+    const int64_t per_wg = std::max<int64_t>(1, (groups * units + 4 * kScoreSlots) / (8 * kScoreSlots));
+    y.pwg = (int32_t)std::min<int64_t>(groups, (groups + per_wg - 1) / per_wg);
   }
   y.nqg = (int32_t)((rows + kStatsRows - 1) / kStatsRows);
   const int64_t base = std::max<int64_t>(1, units * y.nqg);
