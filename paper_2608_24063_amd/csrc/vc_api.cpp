@@ -22,7 +22,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 // Everything derived from (shape, params) on the host.
 struct Layout {
   int32_t B, L, Hq, Hkv, d, W, G, R, h, Ls, mode, vfp32;
-  int32_t nqg, nks, ncol, nfuse, nmax;
+  int32_t nqg, nks, ncol, nmax;
   int32_t prefill, pwg;
   int64_t Ntot;
   std::vector<int32_t> n, k, ns;       // n[B], k[B*L], ns[B*L]
@@ -95,14 +95,12 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   y.Ntot = y.toff[y.B];
   y.orow.assign((size_t)y.L * (y.B + 1), 0);
   y.drow.assign((size_t)y.L * (y.B + 1), 0);
-  int32_t kmax = 0;
   for (int32_t l = 0; l < y.L; ++l)
     for (int32_t b = 0; b < y.B; ++b) {
       const int32_t kk = y.k[(size_t)b * y.L + l];
       const int32_t rr = l < y.h ? y.ns[(size_t)b * y.L + l] - kk : 0;
       y.orow[(size_t)l * (y.B + 1) + b + 1] = y.orow[(size_t)l * (y.B + 1) + b] + (int64_t)y.Hkv * kk;
       y.drow[(size_t)l * (y.B + 1) + b + 1] = y.drow[(size_t)l * (y.B + 1) + b] + (int64_t)y.Hkv * rr;
-      kmax = std::max(kmax, kk);
     }
   y.nmax = *std::max_element(y.n.begin(), y.n.end());
   const int64_t units = (int64_t)y.Ls * y.B * y.Hkv;
@@ -138,7 +136,6 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   const int64_t per_unit = y.prefill ? std::max<int64_t>(y.pwg, (y.nmax + 255) / 256)
                                      : std::max<int64_t>((int64_t)y.nqg * y.nks, y.ncol);
   if (units * per_unit > (int64_t(1) << 24) - 1) return VC_ERR_UNSUPPORTED;
-  y.nfuse = std::max(1, (kmax + kFuseRows - 1) / kFuseRows);
   // Fusion units (layer < h with kept rows), ordered by dropped-row count,
   // descending: every workgroup of a unit walks all of its dropped tiles, so
   // dispatching the longest chains first bounds the tail.
@@ -450,8 +447,8 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   PrunePlan pl{};
   pl.B = y.B; pl.L = y.L; pl.Hq = y.Hq; pl.Hkv = y.Hkv; pl.d = y.d; pl.W = y.W; pl.G = y.G;
   pl.R = y.R; pl.h = y.h; pl.Ls = y.Ls; pl.mode = y.mode; pl.v_fp32 = y.vfp32;
-  pl.nqg = y.nqg; pl.nks = y.nks; pl.ncol = y.ncol; pl.nfuse = y.nfuse; pl.nmax = y.nmax;
-  pl.prefill = y.prefill; pl.pwg = y.pwg;
+  pl.nqg = y.nqg; pl.nks = y.nks; pl.ncol = y.ncol; pl.nmax = y.nmax;
+  pl.pwg = y.pwg;
   pl.nfunits = (int32_t)y.funit.size();
   pl.nfwg = (int32_t)y.fwoff.size() - 1;
   pl.sc = (float)(1.4426950408889634 / std::sqrt((double)y.d));

@@ -55,11 +55,9 @@ struct PrunePlan {
   int32_t v_fp32;     // fused values stored as fp32
   int32_t nqg, nks;   // stats grid: query groups x key splits per unit
   int32_t ncol;       // column-sum chunks per unit (max over sequences)
-  int32_t nfuse;      // fusion tiles per unit (max over units)
   int32_t nfunits;    // units with kept rows
   int32_t nfwg;       // fusion workgroups (persistent; each walks its job list)
   int32_t nmax;       // max n_b
-  int32_t prefill;    // scores from every prefill token (causal) instead of the window
   int32_t pwg;        // prefill: workgroups per unit (each owns every pwg-th 256-row group)
   float sc;           // log2(e) / sqrt(d)
   float tc;           // log2(e) / tau
