@@ -55,6 +55,8 @@ def lib():
             L.orc_gather.argtypes = [i32, i32, vp, vp, vp]
             L.orc_fuse.argtypes = [i32, i32, i32, vp, vp, vp, f64, f64, vp]
             L.orc_attend.argtypes = [i32, i32, vp, vp, vp, f64, vp]
+            L.orc_quant_rows.argtypes = [i32, i32, vp, vp, vp]
+            L.orc_dequant_rows.argtypes = [i32, i32, vp, vp, vp]
             L.orc_prune_unit.argtypes = [i32, i32, i32, vp, vp, vp, i32, i32, f64, f64,
                                          vp, vp, vp, vp, vp]
             _lib = L
@@ -140,6 +142,26 @@ def attend(q: np.ndarray, K: np.ndarray, V: np.ndarray, scale: float) -> np.ndar
     out = np.zeros(q.shape[-1], dtype=np.float64)
     lib().orc_attend(q.shape[-1], K.shape[0], _p(q), _p(K), _p(V), scale, _p(out))
     return out
+
+
+def quant_rows(x: np.ndarray):
+    """4-bit rows: bf16 bits [n][d] -> (codes uint8 [n][d/2], meta fp32 [n][d/32][2] = (scale, lo))."""
+    x = np.ascontiguousarray(x, dtype=np.uint16)
+    n, d = x.shape
+    codes = np.zeros((max(n, 1), d // 2), dtype=np.uint8)
+    meta = np.zeros((max(n, 1), d // 32, 2), dtype=np.float32)
+    lib().orc_quant_rows(n, d, _p(x), _p(codes), _p(meta))
+    return codes[:n], meta[:n]
+
+
+def dequant_rows(codes: np.ndarray, meta: np.ndarray) -> np.ndarray:
+    """Inverse of quant_rows up to the 4-bit grid: bf16 bits [n][d]."""
+    codes = np.ascontiguousarray(codes, dtype=np.uint8)
+    meta = np.ascontiguousarray(meta, dtype=np.float32)
+    n, d = codes.shape[0], codes.shape[1] * 2
+    out = np.zeros((max(n, 1), d), dtype=np.uint16)
+    lib().orc_dequant_rows(n, d, _p(codes), _p(meta), _p(out))
+    return out[:n]
 
 
 def prune_unit(K: np.ndarray, V: np.ndarray, Q: np.ndarray, k: int, n_surv: int,

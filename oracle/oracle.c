@@ -29,6 +29,14 @@ static uint16_t to_bf16(float f) {
   return (uint16_t)((u + 0x7FFFu + lsb) >> 16);
 }
 
+/* bf16 bit pattern -> fp32 (exact). */
+static float bf32(uint16_t h) {
+  uint32_t u = (uint32_t)h << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return f;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Budgets: Eq. (parabolic), its normalisation, RR = p*q*(h/L)*m, Alg. 1.    */
 /* ------------------------------------------------------------------------ */
@@ -351,4 +359,50 @@ void orc_prune_unit(int32_t n, int32_t d, int32_t rows, const uint16_t *K, const
   if (S32) memcpy(S32, s32, sizeof(float) * (size_t)n);
   free(S);
   free(s32);
+}
+
+/* ------------------------------------------------------------------------ */
+/* 4-bit cache rows (reading of the quantisation experiments; see header).    */
+/* ------------------------------------------------------------------------ */
+
+void orc_quant_rows(int32_t n, int32_t d, const uint16_t *x, uint8_t *codes, float *meta) {
+  const int32_t groups = d / 32;
+  for (int32_t r = 0; r < n; ++r) {
+    memset(codes + (size_t)r * (d / 2), 0, (size_t)(d / 2));
+    for (int32_t g = 0; g < groups; ++g) {
+      const uint16_t *xg = x + (size_t)r * d + 32 * g;
+      float lo = bf32(xg[0]), hi = lo;
+      for (int c = 1; c < 32; ++c) {
+        const float v = bf32(xg[c]);
+        if (v < lo) lo = v;
+        if (v > hi) hi = v;
+      }
+      const float range = hi - lo;
+      const float scale = range / 15.0f;
+      meta[((size_t)r * groups + g) * 2] = scale;
+      meta[((size_t)r * groups + g) * 2 + 1] = lo;
+      for (int c = 0; c < 32; ++c) {
+        int code = 0;
+        if (scale > 0.0f) {
+          const float t = (bf32(xg[c]) - lo) / scale;
+          code = (int)rintf(t);
+          if (code < 0) code = 0;
+          if (code > 15) code = 15;
+        }
+        const int ch = 32 * g + c;
+        codes[(size_t)r * (d / 2) + ch / 2] |= (uint8_t)(code << (4 * (ch & 1)));
+      }
+    }
+  }
+}
+
+void orc_dequant_rows(int32_t n, int32_t d, const uint8_t *codes, const float *meta, uint16_t *out) {
+  const int32_t groups = d / 32;
+  for (int32_t r = 0; r < n; ++r)
+    for (int32_t ch = 0; ch < d; ++ch) {
+      const int code = (codes[(size_t)r * (d / 2) + ch / 2] >> (4 * (ch & 1))) & 15;
+      const float scale = meta[((size_t)r * groups + ch / 32) * 2];
+      const float lo = meta[((size_t)r * groups + ch / 32) * 2 + 1];
+      out[(size_t)r * d + ch] = to_bf16(fmaf((float)code, scale, lo));
+    }
 }

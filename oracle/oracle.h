@@ -76,6 +76,20 @@ void orc_fuse(int32_t d, int32_t k, int32_t r, const uint16_t *V, const int32_t 
 void orc_attend(int32_t d, int32_t rows, const uint16_t *q, const uint16_t *K, const uint16_t *V,
                 double scale, double *out);
 
+/* 4-bit cache rows (the combination with 4-bit KV-cache quantisation of the
+ * quantisation experiments; the paper names the quantisers but does not define
+ * them, so this is a reading): every row of a bf16 [n][d] block is split into
+ * d/32 groups of 32 consecutive channels; group g of row r keeps
+ *   lo = min, hi = max of its 32 values (fp32),
+ *   scale = fp32(hi - lo) / 15            (fp32, IEEE rounding),
+ *   code_c = clamp(rint(fp32(x_c - lo) / scale), 0, 15), 0 when scale = 0,
+ * and the row's value is read back as bf16(fma(code_c, scale, lo)).  Every
+ * step is fp32 arithmetic, so the integer codes are fixed bit for bit.
+ * codes: [n][d/2] bytes, channel 2j in the low nibble of byte j, 2j+1 in the
+ * high nibble; meta: [n][d/32][2] fp32 (scale, lo).  d must be a multiple of 32. */
+void orc_quant_rows(int32_t n, int32_t d, const uint16_t *x, uint8_t *codes, float *meta);
+void orc_dequant_rows(int32_t n, int32_t d, const uint8_t *codes, const float *meta, uint16_t *out);
+
 /* One LAYER_HEAD unit end to end: score -> select -> gather -> fuse.
  * S32 (may be NULL) receives the fp32 scores used for the ranking. */
 void orc_prune_unit(int32_t n, int32_t d, int32_t rows, const uint16_t *K, const uint16_t *V,
