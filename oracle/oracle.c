@@ -377,6 +377,7 @@ void orc_quant_rows(int32_t n, int32_t d, const uint16_t *x, uint8_t *codes, flo
         if (v < lo) lo = v;
         if (v > hi) hi = v;
       }
+      lo = lo + 0.0f; /* -0 -> +0: the stored offset does not depend on which zero came first */
       const float range = hi - lo;
       const float scale = range / 15.0f;
       meta[((size_t)r * groups + g) * 2] = scale;

@@ -49,6 +49,19 @@ def test_constant_group(orc):
     np.testing.assert_array_equal(orc.dequant_rows(codes, meta), bits)
 
 
+def test_signed_zero_offset(orc):
+    # A group whose minimum is zero stores +0 as its offset whichever zero
+    # (+0 or -0) comes first, so the stored bits depend only on the values.
+    for first, second in ((0x8000, 0x0000), (0x0000, 0x8000), (0x8000, 0x8000)):
+        x = np.full((1, 32), first, dtype=np.uint16)
+        x[0, 1::2] = second
+        x[0, 5] = _bf16(2.0)
+        c, m = orc.quant_rows(x)
+        assert m[0, 0, 1].view(np.uint32) == 0
+        assert m[0, 0, 0] == np.float32(2.0) / np.float32(15.0)
+        assert _codes(c)[0, 5] == 15 and np.all(np.delete(_codes(c)[0], 5) == 0)
+
+
 def test_nibble_order(orc):
     # Channel 2j is the low nibble of byte j: a ramp 0..15 repeated.
     x = np.tile(np.arange(16, dtype=np.float32), 2)[None, :]
