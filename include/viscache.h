@@ -289,6 +289,51 @@ vc_status viscache_decode_step(const vc_decode_shape *shape, const vc_cache *cac
                                const void *v_new, const void *q, float *out, float scale,
                                int64_t max_rows, void *workspace, size_t workspace_bytes, void *stream);
 
+/* ---- 4-bit cache rows ----------------------------------------------------
+ * The quantisation experiments combine the pruned cache with 4-bit KV-cache
+ * quantisation but do not define the quantiser.  The reading taken here: each
+ * row's d channels form d/32 groups of 32; a group keeps lo = min and
+ * scale = (max - min) / 15 as fp32 and its channels the 4-bit codes
+ * clamp(rint((x - lo) / scale), 0, 15) (0 when scale = 0), all in IEEE fp32;
+ * a row is read back as bf16(fma(code, scale, lo)).  Keys and values alike,
+ * per row, so a tile of rows reads back without any other rows' data.
+ * codes: uint8 [rows][d/2], channel 2j in the low nibble of byte j, 2j+1 in
+ * the high one; meta: fp32 [rows][d/32][2] = (scale, lo). */
+
+/* Device, asynchronous.  Quantises `rows` contiguous bf16 rows of d values
+ * (src, DEVICE [rows][d]) into codes and meta (DEVICE, laid out as above;
+ * the caller owns all three).  src and codes must be 16-byte aligned, meta
+ * 8-byte aligned.  VC_ERR_UNSUPPORTED unless d is 64 or 128; VC_ERR_ARG for
+ * rows < 0 or, with rows > 0, a null or misaligned pointer.  rows = 0 does
+ * nothing. */
+vc_status viscache_quantize_rows(int32_t d, int64_t rows, const void *src, void *codes, void *meta, void *stream);
+
+/* A 4-bit prefix of a decode cache: rows [0, nq[u]) of unit u are read from
+ * the quantised pools at rows qrow_off[u] + i (codes and meta as above, for
+ * keys and values), rows [nq[u], len[u]) from the bf16 pools of the vc_cache
+ * as usual (appended rows always go there).  nq[u] must be a multiple of 32
+ * and at most len[u]; the kernel rounds it down to a multiple of 32 and
+ * clamps it to len[u].  qrow_off (int64) and nq (int32): DEVICE arrays of
+ * L*B*Hkv entries.  All pointers DEVICE. */
+typedef struct {
+  const void *k_codes;
+  const void *k_meta;
+  const void *v_codes;
+  const void *v_meta;
+  const int64_t *qrow_off;
+  const int32_t *nq;
+} vc_qcache;
+
+/* Device, asynchronous.  viscache_decode_step over a cache whose leading rows
+ * are 4-bit (read back as described above before they enter the products);
+ * every other argument, the workspace (viscache_decode_step_workspace_bytes)
+ * and the errors as for viscache_decode_step, plus VC_ERR_ARG for a null
+ * qcache member, code arrays not 4-byte aligned or meta arrays not 8-byte
+ * aligned. */
+vc_status viscache_decode_step_q4(const vc_decode_shape *shape, const vc_cache *cache, const vc_qcache *qcache,
+                                  const void *k_new, const void *v_new, const void *q, float *out, float scale,
+                                  int64_t max_rows, void *workspace, size_t workspace_bytes, void *stream);
+
 /* Static text for a status code. */
 const char *viscache_strerror(vc_status s);
 

@@ -47,6 +47,11 @@ class vc_cache(ctypes.Structure):
     _fields_ = [("k_pool", c_vp), ("v_pool", c_vp), ("row_off", c_vp), ("cap", c_vp), ("len", c_vp)]
 
 
+class vc_qcache(ctypes.Structure):
+    _fields_ = [("k_codes", c_vp), ("k_meta", c_vp), ("v_codes", c_vp), ("v_meta", c_vp),
+                ("qrow_off", c_vp), ("nq", c_vp)]
+
+
 class VisCacheError(RuntimeError):
     def __init__(self, status: int, what: str):
         super().__init__(f"{what}: {strerror(status)} (status {status})")
@@ -83,11 +88,15 @@ def lib() -> ctypes.CDLL:
         L.viscache_decode_step_workspace_bytes.restype = ctypes.c_size_t
         L.viscache_decode_step.argtypes = [P(vc_decode_shape), P(vc_cache), c_vp, c_vp, c_vp, c_vp, c_f32,
                                            c_i64, c_vp, ctypes.c_size_t, c_vp]
+        L.viscache_decode_step_q4.argtypes = [P(vc_decode_shape), P(vc_cache), P(vc_qcache), c_vp, c_vp, c_vp,
+                                              c_vp, c_f32, c_i64, c_vp, ctypes.c_size_t, c_vp]
+        L.viscache_quantize_rows.argtypes = [c_i32, c_i64, c_vp, c_vp, c_vp, c_vp]
         L.viscache_strerror.argtypes = [c_i32]
         L.viscache_strerror.restype = ctypes.c_char_p
         for name in ("viscache_budget", "viscache_out_rows", "viscache_prune", "viscache_prune_score_offsets",
                      "viscache_prune_staged",
-                     "viscache_append_kv", "viscache_decode_attn", "viscache_decode_step"):
+                     "viscache_append_kv", "viscache_decode_attn", "viscache_decode_step",
+                     "viscache_decode_step_q4", "viscache_quantize_rows"):
             getattr(L, name).restype = c_i32
         _lib = L
     return _lib
@@ -231,6 +240,18 @@ def viscache_decode_step(shape: vc_decode_shape, cache: vc_cache, k_new: int, v_
                                       max_rows, workspace, workspace_bytes, stream), "viscache_decode_step")
 
 
+def viscache_decode_step_q4(shape: vc_decode_shape, cache: vc_cache, qcache: vc_qcache, k_new: int,
+                            v_new: int, q: int, out: int, scale: float, max_rows: int, workspace: int,
+                            workspace_bytes: int, stream: int) -> None:
+    _check(lib().viscache_decode_step_q4(ctypes.byref(shape), ctypes.byref(cache), ctypes.byref(qcache), k_new,
+                                         v_new, q, out, scale, max_rows, workspace, workspace_bytes, stream),
+           "viscache_decode_step_q4")
+
+
+def viscache_quantize_rows(d: int, rows: int, src: int, codes: int, meta: int, stream: int) -> None:
+    _check(lib().viscache_quantize_rows(d, rows, src, codes, meta, stream), "viscache_quantize_rows")
+
+
 def viscache_strerror(status: int) -> str:
     return strerror(status)
 
@@ -239,4 +260,4 @@ EXPORTED = ("viscache_default_params", "viscache_budget", "viscache_out_rows",
             "viscache_prune_workspace_bytes", "viscache_prune_score_offsets", "viscache_prune",
             "viscache_prune_staged", "viscache_decode_workspace_bytes",
             "viscache_append_kv", "viscache_decode_attn", "viscache_decode_step_workspace_bytes",
-            "viscache_decode_step", "viscache_strerror")
+            "viscache_decode_step", "viscache_decode_step_q4", "viscache_quantize_rows", "viscache_strerror")

@@ -87,6 +87,48 @@ struct RowTile {
       v[it] = ld16(src + (c % kCpr) * 8);
     }
   }
+  // 4-bit rows (rows t0.. of the unit's quantised block Kc/Km, Vc/Vm): each
+  // 16-byte slot above carries instead the 4 code bytes of its 8 channels and
+  // their group's (scale, lo); unpack() turns them into the bf16 values.
+  __device__ __forceinline__ void load_q(const uint8_t *Kc, const float2 *Km, const uint8_t *Vc, const float2 *Vm,
+                                         int t0, int r1, int lr, int lg, int lane) {
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+      const int64_t row = min(t0 + rb * 16 + lr, r1 - 1);
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const uint32_t c = ldg(reinterpret_cast<const uint32_t *>(Kc + row * (D / 2) + 16 * s + 4 * lg));
+        const float2 m = ldg(Km + row * (D / 32) + s);
+        k[rb][s] = u32x4{c, __float_as_uint(m.x), __float_as_uint(m.y), 0u};
+      }
+    }
+    constexpr int kCpr = D / 8;
+#pragma unroll
+    for (int it = 0; it < kVIt; ++it) {
+      const int c = lane + 64 * it;
+      const int64_t row = min(t0 + c / kCpr, r1 - 1);
+      const int ch = c % kCpr;  // channels 8 ch .. 8 ch + 7, group ch / 4
+      const uint32_t code = ldg(reinterpret_cast<const uint32_t *>(Vc + row * (D / 2) + 4 * ch));
+      const float2 m = ldg(Vm + row * (D / 32) + ch / 4);
+      v[it] = u32x4{code, __float_as_uint(m.x), __float_as_uint(m.y), 0u};
+    }
+  }
+  // bf16(fma(code, scale, lo)) of 8 channels, in channel order.
+  static __device__ __forceinline__ u32x4 deq8(const u32x4 w) {
+    const float sc = __uint_as_float(w.y), lo = __uint_as_float(w.z);
+    float f[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) f[j] = fmaf((float)((w.x >> (4 * j)) & 15u), sc, lo);
+    return u32x4{pack_bf16(f[0], f[1]), pack_bf16(f[2], f[3]), pack_bf16(f[4], f[5]), pack_bf16(f[6], f[7])};
+  }
+  __device__ __forceinline__ void unpack() {
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int s = 0; s < KS; ++s) k[rb][s] = deq8(k[rb][s]);
+#pragma unroll
+    for (int it = 0; it < kVIt; ++it) v[it] = deq8(v[it]);
+  }
 };
 
 // Partials exchanged inside one launch may cross XCDs (separate L2s): they
@@ -295,10 +337,10 @@ enum PieceOut { kPartial = 0, kPartialCoherent = 1, kOutput = 2 };
 // Attention of the query heads of unit u over cache rows [r0, r1) (row nrow,
 // if in range, read from knew / vnew); the result goes to partial slot
 // `slot` or to the output.
-template <int D, int OUT>
+template <int D, int OUT, bool Q4>
 __device__ __forceinline__ void attend_piece(const DecodePlan &p, DecodeSmem<D> &sm, int u, int64_t roff, int slot,
                                              int r0, int r1, int nrow, const uint16_t *knew,
-                                             const uint16_t *vnew) {
+                                             const uint16_t *vnew, int nq, int64_t qoff) {
   constexpr int KS = D / 32;
   constexpr int MB = D / 16;
   constexpr int PR = DecodeSmem<D>::PR;
@@ -333,11 +375,27 @@ __device__ __forceinline__ void attend_piece(const DecodePlan &p, DecodeSmem<D> 
   // Wave w takes tiles w, w+4, ...; the next tile's rows are in flight while
   // the current one is processed.
   const int ntiles = r1 > r0 ? (r1 - r0 + kRowTile - 1) / kRowTile : 0;
+  // Q4: tiles below nq (a multiple of the tile) come from the 4-bit block.
+  const uint8_t *Kc = nullptr, *Vc = nullptr;
+  const float2 *Km = nullptr, *Vm = nullptr;
+  if (Q4) {
+    Kc = p.qk + qoff * (D / 2);
+    Vc = p.qv + qoff * (D / 2);
+    Km = p.qkm + qoff * (D / 32);
+    Vm = p.qvm + qoff * (D / 32);
+  }
+  auto load_tile = [&](RowTile<D> &rt, int tstart) {
+    if (Q4 && tstart < nq)
+      rt.load_q(Kc, Km, Vc, Vm, tstart, nq, lr, lg, lane);
+    else
+      rt.load(Kp, Vp, tstart, r1, lr, lg, lane, nrow, knew, vnew);
+  };
   RowTile<D> cur, nxt;
-  if (w < ntiles) cur.load(Kp, Vp, r0 + w * kRowTile, r1, lr, lg, lane, nrow, knew, vnew);
+  if (w < ntiles) load_tile(cur, r0 + w * kRowTile);
   for (int t = w; t < ntiles; t += 4) {
     const int t0 = r0 + t * kRowTile;
-    if (t + 4 < ntiles) nxt.load(Kp, Vp, t0 + 4 * kRowTile, r1, lr, lg, lane, nrow, knew, vnew);
+    if (t + 4 < ntiles) load_tile(nxt, t0 + 4 * kRowTile);
+    if (Q4 && t0 < nq) cur.unpack();  // wave-uniform
     // S^T = K Q^T for 2 blocks of 16 rows.
     f32x4 acc[2];
 #pragma unroll
@@ -496,7 +554,7 @@ __device__ __forceinline__ void merge_pieces(const DecodePlan &p, int u, int slo
 // Decode attention over the cut (STEP: the fused step, which also appends
 // the new rows, merges each split unit in the last of its workgroups to
 // finish, and advances the unit's length there).
-template <int D, bool STEP>
+template <int D, bool STEP, bool Q4 = false>
 __device__ __forceinline__ void decode_body(const DecodePlan &p) {
   __shared__ DecodeSmem<D> sm;
   // Pieces follow the dispatch order, so the workgroups left without a piece
@@ -532,10 +590,19 @@ __device__ __forceinline__ void decode_body(const DecodePlan &p) {
       stg(reinterpret_cast<int32_t *>(p.pinfo + u), p0);
       stg(reinterpret_cast<int32_t *>(p.pinfo + u) + 1, np);
     }
+    // Q4: the unit's 4-bit rows, a multiple of the tile, within its length.
+    int nq = 0;
+    int64_t qoff = 0;
+    if (Q4) {
+      nq = min(ldg(p.nq + u) & ~(kRowTile - 1), max(pc.len0, 0) & ~(kRowTile - 1));
+      nq = max(nq, 0);
+      qoff = ldg(p.qoff + u);
+    }
     if (np == 1)
-      attend_piece<D, kOutput>(p, sm, u, pc.roff, 0, r0, r1, nrow, knew, vnew);
+      attend_piece<D, kOutput, Q4>(p, sm, u, pc.roff, 0, r0, r1, nrow, knew, vnew, nq, qoff);
     else
-      attend_piece<D, STEP ? kPartialCoherent : kPartial>(p, sm, u, pc.roff, (int)i, r0, r1, nrow, knew, vnew);
+      attend_piece<D, STEP ? kPartialCoherent : kPartial, Q4>(p, sm, u, pc.roff, (int)i, r0, r1, nrow, knew, vnew,
+                                                              nq, qoff);
   }
   if (!STEP || u < 0) return;
   int rows, nrow;
@@ -574,6 +641,12 @@ __global__ __launch_bounds__(256, 2) void k_decode_step(DecodePlan p) {
   decode_body<D, true>(p);
 }
 
+// The fused step over a cache with a 4-bit prefix.
+template <int D>
+__global__ __launch_bounds__(256, 2) void k_decode_step_q4(DecodePlan p) {
+  decode_body<D, true, true>(p);
+}
+
 // Merge the pieces of each split unit (second kernel of the two-call path).
 template <int D>
 __global__ __launch_bounds__(256) void k_decode_combine(DecodePlan p) {
@@ -600,6 +673,15 @@ hipError_t launch_decode_step(const DecodePlan &p, hipStream_t st) {
     hipLaunchKernelGGL(k_decode_step<128>, dim3(p.nwg), dim3(256), 0, st, p);
   else
     hipLaunchKernelGGL(k_decode_step<64>, dim3(p.nwg), dim3(256), 0, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_step_q4(const DecodePlan &p, hipStream_t st) {
+  if (p.units == 0 || p.nwg < 1) return hipSuccess;
+  if (p.d == 128)
+    hipLaunchKernelGGL(k_decode_step_q4<128>, dim3(p.nwg), dim3(256), 0, st, p);
+  else
+    hipLaunchKernelGGL(k_decode_step_q4<64>, dim3(p.nwg), dim3(256), 0, st, p);
   return hipGetLastError();
 }
 

@@ -633,6 +633,51 @@ vc_status viscache_decode_step(const vc_decode_shape *s, const vc_cache *c, cons
   return VC_OK;
 }
 
+vc_status viscache_decode_step_q4(const vc_decode_shape *s, const vc_cache *c, const vc_qcache *qc,
+                                  const void *k_new, const void *v_new, const void *q, float *out, float scale,
+                                  int64_t max_rows, void *workspace, size_t workspace_bytes, void *stream) {
+  DecodePlan p;
+  const vc_status st = decode_plan(s, c, q, out, scale, max_rows, p);
+  if (st != VC_OK) return st;
+  if (!k_new || !v_new || !qc || !qc->k_codes || !qc->k_meta || !qc->v_codes || !qc->v_meta || !qc->qrow_off ||
+      !qc->nq)
+    return VC_ERR_ARG;
+  if ((reinterpret_cast<uintptr_t>(qc->k_codes) | reinterpret_cast<uintptr_t>(qc->v_codes)) % 4 != 0 ||
+      (reinterpret_cast<uintptr_t>(qc->k_meta) | reinterpret_cast<uintptr_t>(qc->v_meta)) % 8 != 0)
+    return VC_ERR_ARG;
+  const size_t need = viscache_decode_step_workspace_bytes(s, max_rows);
+  if (!workspace || workspace_bytes < need) return VC_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return VC_ERR_WORKSPACE;
+  decode_bind_ws(p, static_cast<uint8_t *>(workspace));
+  p.k_pool_w = static_cast<uint16_t *>(c->k_pool);
+  p.v_pool_w = static_cast<uint16_t *>(c->v_pool);
+  p.len_w = c->len;
+  p.k_new = static_cast<const uint16_t *>(k_new);
+  p.v_new = static_cast<const uint16_t *>(v_new);
+  p.qk = static_cast<const uint8_t *>(qc->k_codes);
+  p.qv = static_cast<const uint8_t *>(qc->v_codes);
+  p.qkm = static_cast<const float2 *>(qc->k_meta);
+  p.qvm = static_cast<const float2 *>(qc->v_meta);
+  p.qoff = qc->qrow_off;
+  p.nq = qc->nq;
+  if (launch_decode_step_q4(p, static_cast<hipStream_t>(stream)) != hipSuccess) return VC_ERR_HIP;
+  return VC_OK;
+}
+
+vc_status viscache_quantize_rows(int32_t d, int64_t rows, const void *src, void *codes, void *meta, void *stream) {
+  if (d != 64 && d != 128) return VC_ERR_UNSUPPORTED;
+  if (rows < 0) return VC_ERR_ARG;
+  if (rows == 0) return VC_OK;
+  if (!src || !codes || !meta || (reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(codes)) % 16 != 0 ||
+      reinterpret_cast<uintptr_t>(meta) % 8 != 0)
+    return VC_ERR_ARG;
+  if (rows * (d / 32) > (int64_t)INT32_MAX * 256) return VC_ERR_UNSUPPORTED;
+  if (launch_quant_rows(d, rows, static_cast<const uint16_t *>(src), static_cast<uint8_t *>(codes),
+                        static_cast<float2 *>(meta), static_cast<hipStream_t>(stream)) != hipSuccess)
+    return VC_ERR_HIP;
+  return VC_OK;
+}
+
 const char *viscache_strerror(vc_status s) {
   switch (s) {
     case VC_OK: return "ok";

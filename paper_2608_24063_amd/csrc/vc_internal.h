@@ -145,6 +145,13 @@ struct DecodePlan {
   uint32_t *arrive;
   uint16_t *k_pool_w, *v_pool_w;
   int32_t *len_w;
+  // 4-bit prefix (decode_step_q4 only): codes [rows][d/2], meta [rows][d/32]
+  // (scale, lo) for keys and values, and per unit its first quantised row and
+  // its quantised row count.
+  const uint8_t *qk, *qv;
+  const float2 *qkm, *qvm;
+  const int64_t *qoff;
+  const int32_t *nq;
 };
 
 hipError_t launch_append(int32_t units, int32_t d, uint16_t *k_pool, uint16_t *v_pool,
@@ -152,5 +159,9 @@ hipError_t launch_append(int32_t units, int32_t d, uint16_t *k_pool, uint16_t *v
                          const uint16_t *k_new, const uint16_t *v_new, hipStream_t st);
 hipError_t launch_decode(const DecodePlan &p, hipStream_t st);
 hipError_t launch_decode_step(const DecodePlan &p, hipStream_t st);
+hipError_t launch_decode_step_q4(const DecodePlan &p, hipStream_t st);
+// 4-bit rows: `rows` bf16 rows of d values -> codes [rows][d/2], meta [rows][d/32].
+hipError_t launch_quant_rows(int32_t d, int64_t rows, const uint16_t *src, uint8_t *codes, float2 *meta,
+                             hipStream_t st);
 
 }  // namespace vc

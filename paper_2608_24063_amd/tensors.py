@@ -6,9 +6,10 @@ from __future__ import annotations
 import torch
 
 from . import (VC_PRUNE_EVENTS, VC_RANK_GLOBAL, make_params, make_prune_io, make_shape, prune_with_io, vc_cache,
-               vc_decode_shape, viscache_append_kv, viscache_budget, viscache_decode_attn, viscache_decode_step,
-               viscache_decode_step_workspace_bytes, viscache_decode_workspace_bytes, viscache_out_rows,
-               viscache_prune_workspace_bytes)
+               vc_decode_shape, vc_qcache, viscache_append_kv, viscache_budget, viscache_decode_attn,
+               viscache_decode_step, viscache_decode_step_q4, viscache_decode_step_workspace_bytes,
+               viscache_decode_workspace_bytes, viscache_out_rows, viscache_prune_workspace_bytes,
+               viscache_quantize_rows)
 
 
 def _stream() -> int:
@@ -136,6 +137,30 @@ class DecodeCache:
         viscache_decode_step(self.shape, self.c, k_new.data_ptr(), v_new.data_ptr(), q.data_ptr(),
                              out.data_ptr(), scale, self.max_cap, self.step_ws.data_ptr(), self.step_ws_bytes,
                              _stream())
+
+    def quantize(self, nq) -> None:
+        """Quantise every pool row to 4 bits (viscache_quantize_rows) and let
+        unit u read its first nq[u] rows (rounded down to the 32-row tile)
+        from the codes in later q4 steps; the rows stay in the bf16 pools."""
+        dev = self.k_pool.device
+        rows, d = self.k_pool.shape
+        self.qk = torch.empty((rows, d // 2), dtype=torch.uint8, device=dev)
+        self.qv = torch.empty((rows, d // 2), dtype=torch.uint8, device=dev)
+        self.qkm = torch.empty((rows, d // 32, 2), dtype=torch.float32, device=dev)
+        self.qvm = torch.empty((rows, d // 32, 2), dtype=torch.float32, device=dev)
+        viscache_quantize_rows(d, rows, self.k_pool.data_ptr(), self.qk.data_ptr(), self.qkm.data_ptr(), _stream())
+        viscache_quantize_rows(d, rows, self.v_pool.data_ptr(), self.qv.data_ptr(), self.qvm.data_ptr(), _stream())
+        self.nq = torch.as_tensor([int(x) for x in nq], dtype=torch.int32).to(dev)
+        self.qc = vc_qcache(self.qk.data_ptr(), self.qkm.data_ptr(), self.qv.data_ptr(), self.qvm.data_ptr(),
+                            self.row_off.data_ptr(), self.nq.data_ptr())
+
+    def step_q4(self, k_new: torch.Tensor, v_new: torch.Tensor, q: torch.Tensor, out: torch.Tensor,
+                scale: float) -> None:
+        """step() with each unit's quantised rows read from the 4-bit codes
+        (viscache_decode_step_q4); quantize() first."""
+        viscache_decode_step_q4(self.shape, self.c, self.qc, k_new.data_ptr(), v_new.data_ptr(), q.data_ptr(),
+                                out.data_ptr(), scale, self.max_cap, self.step_ws.data_ptr(), self.step_ws_bytes,
+                                _stream())
 
 
 __all__ = ["PruneCall", "DecodeCache", "make_params"]

@@ -236,3 +236,37 @@ def test_layout_reuse_follows_contents(vc, orc):
     assert vc.viscache_budget(shape, p)[0] == k3
     one = vc.make_shape(1, 28, 28, 4, 128, 64, [3136])  # fewer sequences than the cached plan
     assert vc.viscache_budget(one, p)[0] == k3[:28]
+
+
+def test_q4_arguments(vc):
+    """4-bit entry points: shape, null and alignment checks run on the host."""
+    with pytest.raises(vc.VisCacheError) as ei:
+        vc.viscache_quantize_rows(96, 4, 256, 256, 256, 0)
+    assert ei.value.status == vc.VC_ERR_UNSUPPORTED
+    with pytest.raises(vc.VisCacheError) as ei:
+        vc.viscache_quantize_rows(128, -1, 256, 256, 256, 0)
+    assert ei.value.status == vc.VC_ERR_ARG
+    vc.viscache_quantize_rows(128, 0, 0, 0, 0, 0)  # nothing to do, nothing enqueued
+    for src, codes, meta in ((0, 256, 256), (264, 256, 256), (256, 260, 256), (256, 256, 260)):
+        with pytest.raises(vc.VisCacheError) as ei:
+            vc.viscache_quantize_rows(64, 4, src, codes, meta, 0)
+        assert ei.value.status == vc.VC_ERR_ARG
+    ds = vc.vc_decode_shape(1, 2, 8, 2, 128)
+    c = vc.vc_cache(256, 256, 256, 256, 256)
+    need = vc.viscache_decode_step_workspace_bytes(ds, 100)
+    good = (256, 256, 256, 256, 256, 256)
+    for i in range(6):
+        f = list(good)
+        f[i] = 0
+        with pytest.raises(vc.VisCacheError) as ei:
+            vc.viscache_decode_step_q4(ds, c, vc.vc_qcache(*f), 256, 256, 256, 256, 0.1, 100, 256, need, 0)
+        assert ei.value.status == vc.VC_ERR_ARG
+    for i, bad in ((0, 258), (1, 260), (2, 258), (3, 260)):
+        f = list(good)
+        f[i] = bad
+        with pytest.raises(vc.VisCacheError) as ei:
+            vc.viscache_decode_step_q4(ds, c, vc.vc_qcache(*f), 256, 256, 256, 256, 0.1, 100, 256, need, 0)
+        assert ei.value.status == vc.VC_ERR_ARG
+    with pytest.raises(vc.VisCacheError) as ei:
+        vc.viscache_decode_step_q4(ds, c, vc.vc_qcache(*good), 256, 256, 256, 256, 0.1, 100, 256, need - 1, 0)
+    assert ei.value.status == vc.VC_ERR_WORKSPACE

@@ -1,0 +1,283 @@
+"""GPU parity of the 4-bit cache rows (viscache_quantize_rows) and of decode
+over a cache whose leading rows are 4-bit (viscache_decode_step_q4), through
+the C ABI, against the oracle's quant_rows / dequant_rows / attend.
+
+The codes and the (scale, lo) pairs are integer and IEEE fp32 results of the
+same correctly rounded operations on both sides, so they must agree bit for
+bit; the decode output, an fp32 softmax average, is held to the decode
+tolerance (1e-4 of the row's largest magnitude) against the oracle's fp64
+attention over the read-back rows."""
+import numpy as np
+import pytest
+
+from tests.parity import fused_error
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+TOL = 1e-4
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2608_24063_amd as vc
+    vc.lib()
+    return torch.device("cuda:0")
+
+
+def _bf16_bits(x) -> np.ndarray:
+    """fp32 values -> bf16 bits, truncating the low mantissa bits."""
+    return (np.asarray(x, dtype=np.float32).view(np.uint32) >> 16).astype(np.uint16)
+
+
+def _special_rows(d: int) -> np.ndarray:
+    """Rows that reach the quantiser's degenerate and boundary cases."""
+    rows = []
+    rows.append(np.full(d, 1.5, dtype=np.float32))                 # constant: scale 0, codes 0
+    z = np.zeros(d, dtype=np.float32)
+    z[1::3] = -0.0
+    rows.append(z)                                                   # zeros of both signs
+    g = np.arange(d, dtype=np.float32) % 16 * 0.25 - 1.0             # exactly on the 16-level grid
+    rows.append(g)
+    h = (np.arange(d) % 2).astype(np.float32) * 2 - 1                # two levels
+    rows.append(h)
+    big = np.where(np.arange(d) % 5 == 0, 1e38, -1e38).astype(np.float32)
+    rows.append(big)                                                 # wide but finite range
+    tiny = (np.arange(d) % 7).astype(np.float32) * np.float32(2.0 ** -120)
+    rows.append(tiny)                                                # tiny magnitudes
+    half = np.arange(d, dtype=np.float32) % 32 / 62.0                # many ties near x.5 steps
+    rows.append(half)
+    return np.stack([_bf16_bits(r) for r in rows])
+
+
+@pytest.mark.parametrize("d,rows", [(128, 1), (128, 3001), (64, 257), (64, 4096)])
+def test_quantize_rows_bit_exact(dev, orc, sg, d, rows):
+    """Codes and meta equal the oracle's bit for bit on random rows (plus the
+    special rows), and nothing past the last row is written."""
+    import paper_2608_24063_amd as vc
+    from synthgen.device import bf16_tensor
+    x = sg.normal_bf16(41, d + rows, (rows, d))
+    sp = _special_rows(d)
+    x[:min(rows, len(sp))] = sp[:min(rows, len(sp))]
+    src = bf16_tensor(x, dev)
+    codes = torch.full((rows + 1, d // 2), 0xA5, dtype=torch.uint8, device=dev)
+    meta = torch.full((rows + 1, d // 32, 2), 7.0, dtype=torch.float32, device=dev)
+    vc.viscache_quantize_rows(d, rows, src.data_ptr(), codes.data_ptr(), meta.data_ptr(),
+                              torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    c_ref, m_ref = orc.quant_rows(x)
+    c_got, m_got = codes.cpu().numpy(), meta.cpu().numpy()
+    assert np.array_equal(c_got[:rows], c_ref), "codes differ from the oracle"
+    assert np.array_equal(m_got[:rows].view(np.uint32), m_ref.view(np.uint32)), "meta differs from the oracle"
+    assert np.all(c_got[rows] == 0xA5) and np.all(m_got[rows] == 7.0), "wrote past the last row"
+
+
+def _attend_ref(orc, q, K, V, scale):
+    return orc.attend(q, K, V, scale)
+
+
+def _q4_case(dev, orc, sg, d, Hq, Hkv, lens, nq_req, steps, seed, compact):
+    """Two copies of one cache: one stepped with decode_step_q4 over 4-bit
+    prefixes, the other with plain decode_step.  Checks every step of the
+    q4 copy against the oracle over (read-back prefix | bf16 rows) and that
+    both copies append the same rows."""
+    import paper_2608_24063_amd as vc
+    from paper_2608_24063_amd.tensors import DecodeCache
+    from synthgen.device import bf16_tensor, to_host_bf16
+    L, B = 2, 1
+    units = L * B * Hkv
+    assert len(lens) == units and len(nq_req) == units
+    caps = [x + steps + 1 for x in lens]
+    qc_cache = DecodeCache(L, B, Hq, Hkv, d, caps, dev)
+    ref = DecodeCache(L, B, Hq, Hkv, d, caps, dev)
+    Kp = sg.normal_bf16(seed, 1, (qc_cache.total_rows, d))
+    Vp = sg.normal_bf16(seed, 2, (qc_cache.total_rows, d))
+    for cc in (qc_cache, ref):
+        cc.k_pool.copy_(bf16_tensor(Kp, dev))
+        cc.v_pool.copy_(bf16_tensor(Vp, dev))
+        cc.len.copy_(torch.tensor(lens, dtype=torch.int32))
+    stream = torch.cuda.current_stream().cuda_stream
+    if compact:
+        # Only each unit's requested prefix is quantised, packed unit after
+        # unit in reverse order (qrow_off unrelated to the pool offsets).
+        order = list(range(units))[::-1]
+        qoff, o = [0] * units, 0
+        for u in order:
+            qoff[u] = o
+            o += nq_req[u]
+        nrows = max(o, 1)
+        Kq = np.zeros((nrows, d), dtype=np.uint16)
+        Vq = np.zeros((nrows, d), dtype=np.uint16)
+        for u in order:
+            r0 = qc_cache.offs_host[u]
+            Kq[qoff[u]:qoff[u] + nq_req[u]] = Kp[r0:r0 + nq_req[u]]
+            Vq[qoff[u]:qoff[u] + nq_req[u]] = Vp[r0:r0 + nq_req[u]]
+        qk = torch.empty((nrows, d // 2), dtype=torch.uint8, device=dev)
+        qv = torch.empty_like(qk)
+        qkm = torch.empty((nrows, d // 32, 2), dtype=torch.float32, device=dev)
+        qvm = torch.empty_like(qkm)
+        Kqt, Vqt = bf16_tensor(Kq, dev), bf16_tensor(Vq, dev)
+        vc.viscache_quantize_rows(d, o, Kqt.data_ptr(), qk.data_ptr(), qkm.data_ptr(), stream)
+        vc.viscache_quantize_rows(d, o, Vqt.data_ptr(), qv.data_ptr(), qvm.data_ptr(), stream)
+        qoff_t = torch.tensor(qoff, dtype=torch.int64, device=dev)
+        nq_t = torch.tensor(nq_req, dtype=torch.int32, device=dev)
+        qcs = vc.vc_qcache(qk.data_ptr(), qkm.data_ptr(), qv.data_ptr(), qvm.data_ptr(), qoff_t.data_ptr(),
+                           nq_t.data_ptr())
+        Kd = orc.dequant_rows(*orc.quant_rows(Kq))
+        Vd = orc.dequant_rows(*orc.quant_rows(Vq))
+
+        def prefix(u, n):
+            return Kd[qoff[u]:qoff[u] + n], Vd[qoff[u]:qoff[u] + n]
+
+        def run(k, v, q, out, scale):
+            vc.viscache_decode_step_q4(qc_cache.shape, qc_cache.c, qcs, k.data_ptr(), v.data_ptr(), q.data_ptr(),
+                                       out.data_ptr(), scale, qc_cache.max_cap, qc_cache.step_ws.data_ptr(),
+                                       qc_cache.step_ws_bytes, stream)
+    else:
+        qc_cache.quantize(nq_req)
+        Kd = orc.dequant_rows(*orc.quant_rows(Kp))
+        Vd = orc.dequant_rows(*orc.quant_rows(Vp))
+        c_ref, m_ref = orc.quant_rows(Kp)
+        torch.cuda.synchronize()
+        assert np.array_equal(qc_cache.qk.cpu().numpy(), c_ref)
+        assert np.array_equal(qc_cache.qkm.cpu().numpy().view(np.uint32), m_ref.view(np.uint32))
+
+        def prefix(u, n):
+            r0 = qc_cache.offs_host[u]
+            return Kd[r0:r0 + n], Vd[r0:r0 + n]
+
+        def run(k, v, q, out, scale):
+            qc_cache.step_q4(k, v, q, out, scale)
+    scale = d ** -0.5
+    cur = list(lens)
+    G = Hq // Hkv
+    for t in range(steps):
+        kn = sg.normal_bf16(seed + 1 + t, 1, (L, B, Hkv, d))
+        vn = sg.normal_bf16(seed + 1 + t, 2, (L, B, Hkv, d))
+        q = sg.normal_bf16(seed + 1 + t, 3, (L, B, Hq, d))
+        kt, vt, qt = bf16_tensor(kn, dev), bf16_tensor(vn, dev), bf16_tensor(q, dev)
+        out = torch.full((L, B, Hq, d), float("nan"), dtype=torch.float32, device=dev)
+        out_r = torch.full((L, B, Hq, d), float("nan"), dtype=torch.float32, device=dev)
+        # What the kernel reads from the codes: nq rounded down to the tile
+        # and clamped to the length at the call.
+        nq_eff = [min(n // 32 * 32, L0 // 32 * 32) for n, L0 in zip(nq_req, cur)]
+        run(kt, vt, qt, out, scale)
+        ref.step(kt, vt, qt, out_r, scale)
+        torch.cuda.synchronize()
+        cur = [min(x + 1, cap) for x, cap in zip(cur, caps)]
+        assert qc_cache.len.cpu().tolist() == cur == ref.len.cpu().tolist()
+        assert torch.equal(qc_cache.k_pool, ref.k_pool) and torch.equal(qc_cache.v_pool, ref.v_pool)
+        if all(n == 0 for n in nq_eff):
+            assert torch.equal(out, out_r), f"step {t}: no 4-bit rows, yet differs from decode_step"
+        K, V, o = to_host_bf16(qc_cache.k_pool), to_host_bf16(qc_cache.v_pool), out.cpu().numpy()
+        for u in range(units):
+            l, g = u // Hkv, u % Hkv
+            r0, n, nq = qc_cache.offs_host[u], cur[u], nq_eff[u]
+            kq, vq = prefix(u, nq)
+            Ku = np.concatenate([kq, K[r0 + nq:r0 + n]])
+            Vu = np.concatenate([vq, V[r0 + nq:r0 + n]])
+            for hh in sorted({0, G // 2, G - 1}):
+                h = g * G + hh
+                ref_o = _attend_ref(orc, q[l, 0, h], Ku, Vu, scale)
+                err = fused_error(ref_o[None, :], o[l, 0, h][None, :])
+                assert err <= TOL, f"step {t} u={u} h={h} n={n} nq={nq}: error {err}"
+    return qc_cache
+
+
+@pytest.mark.parametrize("d,Hq,Hkv", [(128, 8, 2), (64, 28, 4)])
+def test_decode_step_q4_compact_block(dev, orc, sg, d, Hq, Hkv):
+    """Prefixes packed in a block of their own: nq of 0, one tile, a whole
+    length, more than the length (clamped), not a tile multiple (rounded
+    down), and long units whose 4-bit tiles are split over workgroups."""
+    units = 2 * Hkv
+    lens = [64, 1023, 5000, 31, 2049, 96, 3000, 40][:units]
+    nq = [0, 1000, 4992, 33, 2048, 96, 2999, 32][:units]
+    _q4_case(dev, orc, sg, d, Hq, Hkv, lens, nq, steps=3, seed=51, compact=True)
+
+
+@pytest.mark.parametrize("d,Hq,Hkv", [(128, 28, 4), (64, 8, 2)])
+def test_decode_step_q4_whole_pool(dev, orc, sg, d, Hq, Hkv):
+    """DecodeCache.quantize over the whole pool (qrow_off = row offsets)."""
+    units = 2 * Hkv
+    lens = [300, 4097, 33, 1024, 1, 640, 2500, 0][:units]
+    nq = [288, 4096, 32, 1024, 0, 640, 2496, 0][:units]
+    _q4_case(dev, orc, sg, d, Hq, Hkv, lens, nq, steps=2, seed=61, compact=False)
+
+
+def test_decode_step_q4_without_prefix_equals_step(dev, orc, sg):
+    """nq = 0 everywhere: the same output as decode_step, bit for bit."""
+    lens = [0, 1, 31, 2047]
+    _q4_case(dev, orc, sg, 128, 8, 2, lens, [0] * 4, steps=2, seed=71, compact=False)
+
+
+def test_decode_over_pruned_quantised_cache(dev, orc, sg):
+    """prune -> kept rows quantised to 4 bits (whole tiles), text window and
+    generated rows in bf16 -> decode_step_q4 for a few steps, against the
+    oracle over the read-back rows."""
+    import paper_2608_24063_amd as vc
+    from paper_2608_24063_amd.tensors import DecodeCache, PruneCall
+    from synthgen.device import bf16_tensor, to_host_bf16, upload_layers
+    w = sg.TINY
+    n = [int(x) for x in w.n_vis()]
+    params = vc.make_params(w.retention)
+    dv, _ = upload_layers(w, range(w.L), dev, keep_host=True)
+    pc = PruneCall(w.B, w.L, w.Hq, w.Hkv, w.d, w.W, n, params, [dv["K"][l] for l in range(w.L)],
+                   [dv["V"][l] for l in range(w.L)], [dv["Q"][l] for l in range(w.L)])
+    pc.run()
+    steps = 3
+    caps, kept = [], []
+    for l in range(w.L):
+        for b in range(w.B):
+            for g in range(w.Hkv):
+                k = pc.k[b * w.L + l]
+                kept.append(k)
+                caps.append(k + w.W + steps)
+    c = DecodeCache(w.L, w.B, w.Hq, w.Hkv, w.d, caps, dev)
+    text_k = sg.normal_bf16(w.seed, 11, (len(caps), w.W, w.d))
+    text_v = sg.normal_bf16(w.seed, 12, (len(caps), w.W, w.d))
+    lens = []
+    for l in range(w.L):
+        for b in range(w.B):
+            for g in range(w.Hkv):
+                u = (l * w.B + b) * w.Hkv + g
+                r0, k = c.offs_host[u], kept[u]
+                if k:
+                    a0, a1 = pc.unit_rows(l, b, g)
+                    c.k_pool[r0:r0 + k] = pc.k_out[l][a0:a1]
+                    c.v_pool[r0:r0 + k] = pc.v_out[l][a0:a1]
+                c.k_pool[r0 + k:r0 + k + w.W] = bf16_tensor(text_k[u], dev)
+                c.v_pool[r0 + k:r0 + k + w.W] = bf16_tensor(text_v[u], dev)
+                lens.append(k + w.W)
+    c.len.copy_(torch.tensor(lens, dtype=torch.int32))
+    nq = [k // 32 * 32 for k in kept]
+    assert any(nq)
+    c.quantize(nq)
+    torch.cuda.synchronize()
+    K0, V0 = to_host_bf16(c.k_pool), to_host_bf16(c.v_pool)
+    Kd = orc.dequant_rows(*orc.quant_rows(K0))
+    Vd = orc.dequant_rows(*orc.quant_rows(V0))
+    scale = w.d ** -0.5
+    out = torch.empty((w.L, w.B, w.Hq, w.d), dtype=torch.float32, device=dev)
+    for t in range(steps):
+        kn = sg.normal_bf16(w.seed, 200 + 3 * t, (w.L, w.B, w.Hkv, w.d))
+        vn = sg.normal_bf16(w.seed, 201 + 3 * t, (w.L, w.B, w.Hkv, w.d))
+        q = sg.normal_bf16(w.seed, 202 + 3 * t, (w.L, w.B, w.Hq, w.d))
+        c.step_q4(bf16_tensor(kn, dev), bf16_tensor(vn, dev), bf16_tensor(q, dev), out, scale)
+        torch.cuda.synchronize()
+        K, V, o = to_host_bf16(c.k_pool), to_host_bf16(c.v_pool), out.cpu().numpy()
+        ln = c.len.cpu().numpy()
+        for l in range(w.L):
+            for b in range(w.B):
+                for g in range(w.Hkv):
+                    u = (l * w.B + b) * w.Hkv + g
+                    assert ln[u] == lens[u] + t + 1
+                    r0, m = c.offs_host[u], nq[u]
+                    Ku = np.concatenate([Kd[r0:r0 + m], K[r0 + m:r0 + ln[u]]])
+                    Vu = np.concatenate([Vd[r0:r0 + m], V[r0 + m:r0 + ln[u]]])
+                    for hh in (0, w.G - 1):
+                        h = g * w.G + hh
+                        ref_o = orc.attend(q[l, b, h], Ku, Vu, scale)
+                        err = fused_error(ref_o[None, :], o[l, b, h][None, :])
+                        assert err <= TOL, f"step {t} l={l} b={b} h={h}: error {err}"
