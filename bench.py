@@ -11,7 +11,8 @@ input would otherwise be served from the Infinity Cache.
 
 Prints one JSON line: compression throughput (GB of input visual K+V per second)
 with the roofline of the dominant kernel, decode-attention latency per step on
-the full, pruned and empty (no visual rows) caches, and the CPU oracle timed
+the full, pruned, pruned-with-4-bit-kept-rows and empty (no visual rows)
+caches, and the CPU oracle timed
 on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -288,7 +289,8 @@ def time_prune(pc, steps, warmup, flush_buf, torch):
 
 def decode_latency(w, pc, dev, steps, flush_buf, torch, sg):
     """Per-step latency of append + attention over all layers, on the full,
-    pruned and empty-visual caches."""
+    pruned and empty-visual caches, and on the pruned cache with its kept rows
+    in 4 bits (whole 32-row tiles; text and generated rows in bf16)."""
     from paper_2608_24063_amd.tensors import DecodeCache
     from synthgen.device import bf16_tensor
     L, B, Hkv, d = w.L, w.B, w.Hkv, w.d
@@ -300,14 +302,14 @@ def decode_latency(w, pc, dev, steps, flush_buf, torch, sg):
     vn = bf16_tensor(sg.normal_bf16(w.seed, 904, (steps, L, B, Hkv, d)), dev)
     q = bf16_tensor(sg.normal_bf16(w.seed, 905, (steps, L, B, w.Hq, d)), dev)
     out = torch.empty((L, B, w.Hq, d), dtype=torch.float32, device=dev)
-    for variant in ("full", "pruned", "empty"):
+    for variant in ("full", "pruned", "empty", "pruned_q4"):
         vis = []
         for l in range(L):
             for b in range(B):
                 for g in range(Hkv):
                     if variant == "full":
                         vis.append(n[b])
-                    elif variant == "pruned":
+                    elif variant in ("pruned", "pruned_q4"):
                         vis.append(pc.k[b * L + l])
                     else:
                         vis.append(0)
@@ -326,7 +328,7 @@ def decode_latency(w, pc, dev, steps, flush_buf, torch, sg):
                         s0 = toff[b] * Hkv + g * n[b]
                         c.k_pool[r0:r0 + v] = pc.k_in[l][s0:s0 + v]
                         c.v_pool[r0:r0 + v] = pc.v_in[l][s0:s0 + v]
-                    elif variant == "pruned" and v:
+                    elif variant in ("pruned", "pruned_q4") and v:
                         a0, a1 = pc.unit_rows(l, b, g)
                         c.k_pool[r0:r0 + v] = pc.k_out[l][a0:a1]
                         c.v_pool[r0:r0 + v] = pc.v_out[l][a0:a1]
@@ -335,6 +337,11 @@ def decode_latency(w, pc, dev, steps, flush_buf, torch, sg):
                     lens.append(v + w.W)
         c.len.copy_(torch.tensor(lens, dtype=torch.int32))
         rows0 = sum(lens)
+        nq = [v // 32 * 32 for v in vis] if variant == "pruned_q4" else [0] * len(vis)
+        step = c.step
+        if variant == "pruned_q4":
+            c.quantize(nq)
+            step = c.step_q4
         ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
               for _ in range(steps)]
         # one warm-up step on a copy of the lengths, then restore
@@ -343,15 +350,17 @@ def decode_latency(w, pc, dev, steps, flush_buf, torch, sg):
             if flush_buf is not None:
                 flush_buf.sum()
             ev[t][0].record()
-            c.step(kn[t], vn[t], q[t], out, d ** -0.5)  # append + attend, one launch
+            step(kn[t], vn[t], q[t], out, d ** -0.5)  # append + attend, one launch
             ev[t][1].record()
         torch.cuda.synchronize()
         ts = sorted(a.elapsed_time(b) * 1e3 for a, b in ev)
-        bytes_step0 = (rows0 + len(lens)) * d * 2 * 2
+        # K and V: bf16 rows 2d bytes, 4-bit rows d/2 code bytes + d/32 (scale, lo) pairs
+        q4_rows = sum(nq)
+        bytes_step0 = ((rows0 + len(lens) - q4_rows) * d * 2 + q4_rows * (d // 2 + d // 32 * 8)) * 2
         results[variant] = dict(mean_us=sum(ts) / len(ts), median_us=ts[len(ts) // 2],
                                 rows=rows0, bytes_per_step=bytes_step0)
         del c
-    full, pr, em = results["full"], results["pruned"], results["empty"]
+    full, pr, em, pq = results["full"], results["pruned"], results["empty"], results["pruned_q4"]
     rho = pr["bytes_per_step"] / full["bytes_per_step"]
     bound = rho * full["median_us"] + em["median_us"]
     return dict(steps=steps, full_us=full["median_us"], pruned_us=pr["median_us"], empty_us=em["median_us"],
@@ -360,6 +369,10 @@ def decode_latency(w, pc, dev, steps, flush_buf, torch, sg):
                 target_speedup=full["median_us"] / bound, meets_target=pr["median_us"] <= bound,
                 full_hbm_gbs=full["bytes_per_step"] / (full["median_us"] * 1e3),
                 pruned_hbm_gbs=pr["bytes_per_step"] / (pr["median_us"] * 1e3),
+                pruned_q4_us=pq["median_us"], pruned_q4_mean_us=pq["mean_us"],
+                speedup_q4=full["median_us"] / pq["median_us"],
+                q4_bytes_ratio=pq["bytes_per_step"] / pr["bytes_per_step"],
+                pruned_q4_hbm_gbs=pq["bytes_per_step"] / (pq["median_us"] * 1e3),
                 cold=flush_buf is not None)
 
 
@@ -480,7 +493,7 @@ def main():
     dec = None
     if not args.no_decode:
         dsteps = args.decode_steps or w.decode_steps
-        print(f"[bench] decode: {dsteps} steps x 3 caches", file=sys.stderr, flush=True)
+        print(f"[bench] decode: {dsteps} steps x 4 caches", file=sys.stderr, flush=True)
         dec = decode_latency(w, pc, dev, dsteps, flush, torch, sg)
     cpu = None
     if not args.no_cpu_baseline:

@@ -87,47 +87,59 @@ struct RowTile {
       v[it] = ld16(src + (c % kCpr) * 8);
     }
   }
-  // 4-bit rows (rows t0.. of the unit's quantised block Kc/Km, Vc/Vm): each
-  // 16-byte slot above carries instead the 4 code bytes of its 8 channels and
-  // their group's (scale, lo); unpack() turns them into the bf16 values.
+  // 4-bit rows t0.. of the unit's quantised block Kc/Km, Vc/Vm.  K: lane
+  // (lr, lg) takes the codes of channels 32 lg .. 32 lg + 31 (d = 128; 16 lg
+  // .. 16 lg + 15 for d = 64) of its row, all in one group, into k[rb][0] and
+  // the group's (scale, lo) into k[rb][1]; the products then pair them with
+  // the query in the same channel order.  V: lane takes whole groups (row,
+  // group) = lane + 64 it, codes in v[2 it], (scale, lo) in v[2 it + 1].
+  static constexpr int kG = D / 32;        // groups per row
+  static constexpr int kVG = 32 * kG / 64; // V groups per lane
   __device__ __forceinline__ void load_q(const uint8_t *Kc, const float2 *Km, const uint8_t *Vc, const float2 *Vm,
                                          int t0, int r1, int lr, int lg, int lane) {
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
       const int64_t row = min(t0 + rb * 16 + lr, r1 - 1);
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        const uint32_t c = ldg(reinterpret_cast<const uint32_t *>(Kc + row * (D / 2) + 16 * s + 4 * lg));
-        const float2 m = ldg(Km + row * (D / 32) + s);
-        k[rb][s] = u32x4{c, __float_as_uint(m.x), __float_as_uint(m.y), 0u};
+      const float2 m = ldg(Km + row * kG + lg * kG / 4);
+      if (D == 128) {
+        k[rb][0] = ld16(Kc + row * (D / 2) + 16 * lg);
+      } else {
+        const u32x2 c = ld8(Kc + row * (D / 2) + 8 * lg);
+        k[rb][0] = u32x4{c.x, c.y, 0u, 0u};
       }
+      k[rb][1] = u32x4{__float_as_uint(m.x), __float_as_uint(m.y), 0u, 0u};
     }
-    constexpr int kCpr = D / 8;
 #pragma unroll
-    for (int it = 0; it < kVIt; ++it) {
-      const int c = lane + 64 * it;
-      const int64_t row = min(t0 + c / kCpr, r1 - 1);
-      const int ch = c % kCpr;  // channels 8 ch .. 8 ch + 7, group ch / 4
-      const uint32_t code = ldg(reinterpret_cast<const uint32_t *>(Vc + row * (D / 2) + 4 * ch));
-      const float2 m = ldg(Vm + row * (D / 32) + ch / 4);
-      v[it] = u32x4{code, __float_as_uint(m.x), __float_as_uint(m.y), 0u};
+    for (int it = 0; it < kVG; ++it) {
+      const int gi = lane + 64 * it;
+      const int64_t row = min(t0 + gi / kG, r1 - 1);
+      const int grp = gi % kG;
+      const float2 m = ldg(Vm + row * kG + grp);
+      v[2 * it] = ld16(Vc + row * (D / 2) + 16 * grp);
+      v[2 * it + 1] = u32x4{__float_as_uint(m.x), __float_as_uint(m.y), 0u, 0u};
     }
   }
-  // bf16(fma(code, scale, lo)) of 8 channels, in channel order.
-  static __device__ __forceinline__ u32x4 deq8(const u32x4 w) {
-    const float sc = __uint_as_float(w.y), lo = __uint_as_float(w.z);
+  // bf16(fma(code, scale, lo)) of the 8 codes of one word, in channel order.
+  static __device__ __forceinline__ u32x4 deq8(uint32_t w, float sc, float lo) {
+    const uint32_t e = w & 0x0F0F0F0Fu, o = (w >> 4) & 0x0F0F0F0Fu;  // even / odd channels, one per byte
     float f[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) f[j] = fmaf((float)((w.x >> (4 * j)) & 15u), sc, lo);
+    for (int j = 0; j < 4; ++j) {
+      f[2 * j] = fmaf((float)((e >> (8 * j)) & 0xFFu), sc, lo);
+      f[2 * j + 1] = fmaf((float)((o >> (8 * j)) & 0xFFu), sc, lo);
+    }
     return u32x4{pack_bf16(f[0], f[1]), pack_bf16(f[2], f[3]), pack_bf16(f[4], f[5]), pack_bf16(f[6], f[7])};
   }
-  __device__ __forceinline__ void unpack() {
+  // K of a 4-bit tile into bf16 operands: k[rb][s] = chunk lg * KS + s.
+  __device__ __forceinline__ void unpack_k() {
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb)
+    for (int rb = 0; rb < 2; ++rb) {
+      const u32x4 c = k[rb][0];
+      const float sc = __uint_as_float(k[rb][1].x), lo = __uint_as_float(k[rb][1].y);
+      const uint32_t w[4] = {c.x, c.y, c.z, c.w};
 #pragma unroll
-      for (int s = 0; s < KS; ++s) k[rb][s] = deq8(k[rb][s]);
-#pragma unroll
-    for (int it = 0; it < kVIt; ++it) v[it] = deq8(v[it]);
+      for (int s = 0; s < KS; ++s) k[rb][s] = deq8(w[s], sc, lo);
+    }
   }
 };
 
@@ -361,6 +373,17 @@ __device__ __forceinline__ void attend_piece(const DecodePlan &p, DecodeSmem<D> 
     if (lr < p.G) v = ld16(q + 32 * s + 8 * lg);
     bq[s] = as_bf16x8(v);
   }
+  // Q4: the query in the channel order of the 4-bit K operands (chunk
+  // lg * KS + s in block s).
+  bf16x8 bqp[Q4 ? KS : 1];
+  if (Q4) {
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      u32x4 v = {0, 0, 0, 0};
+      if (lr < p.G) v = ld16(q + 8 * (lg * KS + s));
+      bqp[s] = as_bf16x8(v);
+    }
+  }
 
   f32x4 O[MB];
 #pragma unroll
@@ -395,17 +418,41 @@ __device__ __forceinline__ void attend_piece(const DecodePlan &p, DecodeSmem<D> 
   for (int t = w; t < ntiles; t += 4) {
     const int t0 = r0 + t * kRowTile;
     if (t + 4 < ntiles) load_tile(nxt, t0 + 4 * kRowTile);
-    if (Q4 && t0 < nq) cur.unpack();  // wave-uniform
+    const bool qt = Q4 && t0 < nq;  // wave-uniform
     // S^T = K Q^T for 2 blocks of 16 rows.
     f32x4 acc[2];
+    if (qt) {
+      cur.unpack_k();
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-      acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int rb = 0; rb < 2; ++rb) {
+        acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int s = 0; s < KS; ++s) acc[rb] = mfma_bf16(as_bf16x8(cur.k[rb][s]), bq[s], acc[rb]);
+        for (int s = 0; s < KS; ++s) acc[rb] = mfma_bf16(as_bf16x8(cur.k[rb][s]), bqp[Q4 ? s : 0], acc[rb]);
+      }
+    } else {
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+        acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < KS; ++s) acc[rb] = mfma_bf16(as_bf16x8(cur.k[rb][s]), bq[s], acc[rb]);
+      }
     }
-    // V rows -> per-wave LDS tile, row-major (read back transposed below).
-    {
+    // V rows -> per-wave LDS tile, row-major (read back transposed below);
+    // 4-bit groups are read back on the way.
+    if (qt) {
+      constexpr int kG = RowTile<D>::kG;
+#pragma unroll
+      for (int it = 0; it < RowTile<D>::kVG; ++it) {
+        const int gi = lane + 64 * it;
+        const u32x4 c = cur.v[2 * it];
+        const float vs = __uint_as_float(cur.v[2 * it + 1].x), vl = __uint_as_float(cur.v[2 * it + 1].y);
+        uint16_t *dst = myvt + (gi / kG) * PR + (gi % kG) * 32;
+        *reinterpret_cast<u32x4 *>(dst) = RowTile<D>::deq8(c.x, vs, vl);
+        *reinterpret_cast<u32x4 *>(dst + 8) = RowTile<D>::deq8(c.y, vs, vl);
+        *reinterpret_cast<u32x4 *>(dst + 16) = RowTile<D>::deq8(c.z, vs, vl);
+        *reinterpret_cast<u32x4 *>(dst + 24) = RowTile<D>::deq8(c.w, vs, vl);
+      }
+    } else {
       constexpr int kCpr = D / 8;
 #pragma unroll
       for (int it = 0; it < RowTile<D>::kVIt; ++it) {
