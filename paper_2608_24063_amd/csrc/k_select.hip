@@ -230,8 +230,11 @@ __global__ __launch_bounds__(kThreads) void k_select(PrunePlan p) {
 hipError_t launch_select(const PrunePlan &p, hipStream_t st) {
   const uint32_t grid = (uint32_t)p.h * p.B * p.Hkv;
   if (grid == 0) return hipSuccess;
-  // Smallest register run that holds the longest sequence.
-  if (p.nmax <= 256 * 16)
+  // 256 threads hold up to 8 scores each, then 512 and 1024 threads up to 16,
+  // then 1024 threads up to 32.  Fewer scores per thread shorten each radix
+  // pass; more waves lengthen the histogram scans, so 512 threads beat both
+  // 256 and 1024 at 3136 keys (measured).
+  if (p.nmax <= 256 * 8)
     hipLaunchKernelGGL((k_select<256, 16>), dim3(grid), dim3(256), 0, st, p);
   else if (p.nmax <= 512 * 16)
     hipLaunchKernelGGL((k_select<512, 16>), dim3(grid), dim3(512), 0, st, p);
