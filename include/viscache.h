@@ -116,8 +116,11 @@ typedef struct {
  * sequence), B sequences with n_vis[b] visual tokens each.
  * VC_ERR_UNSUPPORTED beyond the kernels' limits: d, (Hq/Hkv)*W > 1024 with
  * window scores, (Hq/Hkv)*(n_vis[b] + W) > 2^26 with prefill scores,
- * n_vis[b] > 32768, or 64*L + 12*B + 16 > 30720 (the layer table and the
- * per-sequence offsets must fit the first 30 KB of the launch plan). */
+ * n_vis[b] > 32768, 64*L + 12*B + 16 > 30720 (the layer table and the
+ * per-sequence offsets must fit the first 30 KB of the launch plan), a score
+ * grid of 2^24 or more workgroups (Ls*B*Hkv units, Ls = h or L, times the
+ * workgroups per unit), or 2^23 or more units (layer < h, sequence, kv head)
+ * with kept tokens (the fusion job code holds a unit's rank in 23 bits). */
 typedef struct {
   int32_t B, L, Hq, Hkv, d, W;
   const int32_t *n_vis; /* HOST array [B]; each entry in [0, 32768] */

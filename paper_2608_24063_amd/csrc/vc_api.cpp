@@ -144,6 +144,9 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
     for (int32_t b = 0; b < y.B; ++b)
       if (y.k[(size_t)b * y.L + l] > 0)
         for (int32_t g = 0; g < y.Hkv; ++g) y.funit.push_back((l * y.B + b) * y.Hkv + g);
+  // A fusion job is one int32, unit rank << 8 | 128-row tile (a unit has at
+  // most 32768 / 128 = 256 tiles), so the ranks must stay below 2^23.
+  if (y.funit.size() >= (size_t(1) << 23)) return VC_ERR_UNSUPPORTED;
   auto drops = [&](int32_t u) {
     const int32_t l = u / (y.Hkv * y.B), b = (u / y.Hkv) % y.B;
     return y.ns[(size_t)b * y.L + l] - y.k[(size_t)b * y.L + l];

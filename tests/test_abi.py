@@ -270,3 +270,19 @@ def test_q4_arguments(vc):
     with pytest.raises(vc.VisCacheError) as ei:
         vc.viscache_decode_step_q4(ds, c, vc.vc_qcache(*good), 256, 256, 256, 256, 0.1, 100, 256, need - 1, 0)
     assert ei.value.status == vc.VC_ERR_WORKSPACE
+
+
+def test_fusion_unit_rank_limit(vc):
+    """A fusion job packs a unit's rank into 23 bits: 2^23 units with kept
+    tokens are refused on the host, one fewer is accepted."""
+    def status(Hkv):
+        # L = h = 2, RR = 1, m = 1: both layers keep all 4 tokens of every head
+        shape = vc.make_shape(1, 2, Hkv, Hkv, 64, 1, [4])
+        try:
+            vc.viscache_budget(shape, vc.make_params(1.0, h=2, m=1.0))
+        except vc.VisCacheError as e:
+            return e.status
+        return vc.VC_OK
+
+    assert status(1 << 22) == vc.VC_ERR_UNSUPPORTED       # 2 * 2^22 = 2^23 units
+    assert status((1 << 22) - 1) == vc.VC_OK              # 2^23 - 2 units

@@ -1,9 +1,8 @@
 """GPU parity of viscache_prune against the oracle, through the C ABI.
 
-Small workloads are compared unit by unit in full; the full-size workloads run
-in the benchmark's launch configuration and are compared on sampled units
-(each unit is independent in the layer/head ranking) plus properties that hold
-at any size."""
+Small workloads and the 7B shape are compared unit by unit in full; the
+long-video, 72B and batched workloads at full size are in
+test_gpu_fullsize.py."""
 import json
 import os
 
@@ -356,71 +355,6 @@ def test_vllm7b_global_full(dev, orc, sg):
             s, _ = r.check_unit(orc, l, 0, g, S32=s32)
             swaps += s
     _diag(dict(workload=w.name, mode=1, swaps=swaps))
-
-
-# -------------------------------------------------- full sizes, sampled units
-def _sample_units(r):
-    w = r.w
-    bs = sorted({0, w.B - 1, int(np.argmin(r.n)), int(np.argmax(r.n))})
-    ls = sorted({0, r.h // 2, r.h - 1})
-    out = []
-    for i, b in enumerate(bs):
-        for j, l in enumerate(ls):
-            out.append((l, b, (i + j) % w.Hkv))
-    return out
-
-
-@pytest.mark.parametrize("name", ["longvideo", "vllm72b", "batched"])
-def test_full_size_sampled(dev, orc, sg, name):
-    r = Run(sg.WORKLOADS[name], dev)
-    r.check_all_layer_head(orc, _sample_units(r))
-    # properties over every unit: counts, ordering, bit copies of kept keys
-    w = r.w
-    for l in range(r.h):
-        for b in range(w.B):
-            for g in range(w.Hkv):
-                kept, drop, krows, _ = r.gpu_unit(l, b, g)
-                k, ns = r.k[b * w.L + l], r.ns[b * w.L + l]
-                assert len(kept) == k and len(drop) == ns - k
-                assert np.all(np.diff(kept) > 0)
-                if g == 0 and b == 0 and l % 5 == 0:
-                    np.testing.assert_array_equal(krows, r.unit_kv("K", l, b, g)[kept])
-                # the kept set is the exact top-k of the GPU's own scores
-                S = r.gpu_scores(l, b, g)
-                assert check_sets(S, k, ns, kept, drop) == 0
-
-
-@pytest.mark.parametrize("name", ["longvideo", "vllm72b", "batched"])
-def test_full_size_global_properties(dev, orc, sg, name):
-    r = Run(sg.WORKLOADS[name], dev, mode=1)
-    w = r.w
-    ntot = int(r.toff[-1])
-    # shared score = fixed-order sum of the per-unit scores
-    ref = np.zeros(ntot)
-    for l in range(w.L):
-        for b in range(w.B):
-            for g in range(w.Hkv):
-                nb = r.n[b]
-                ref[r.toff[b]:r.toff[b] + nb] += r.gpu_scores(l, b, g)
-    assert rel_err(ref, r.gs, floor=1e-30) < 1e-6
-    # sampled per-unit scores against the oracle
-    for (l, b, g) in _sample_units(r)[:3]:
-        S32 = orc.scores_unit(r.unit_kv("K", l, b, g), r.unit_q(l, b, g))
-        assert rel_err(S32, r.gpu_scores(l, b, g), floor=1e-30) < 1e-4
-    # selection is the exact top-k of the shared score, for every unit
-    for b in range(w.B):
-        gs = r.gs[r.toff[b]:r.toff[b] + r.n[b]]
-        for l in range(r.h):
-            for g in range(w.Hkv):
-                kept, drop, _, _ = r.gpu_unit(l, b, g)
-                assert check_sets(gs, r.k[b * w.L + l], r.ns[b * w.L + l], kept, drop) == 0
-    # fused values of sampled units against the oracle on the GPU's sets
-    for (l, b, g) in _sample_units(r)[:4]:
-        kept, drop, krows, vrows = r.gpu_unit(l, b, g)
-        V = r.unit_kv("V", l, b, g)
-        ref = orc.fuse(V, kept.astype(np.int32), drop.astype(np.int32))
-        assert fused_error(ref, vrows) <= TOL_BF16
-        np.testing.assert_array_equal(krows, r.unit_kv("K", l, b, g)[kept])
 
 
 # ----------------------- prefill scores: every prefill token queries, causally
