@@ -138,6 +138,28 @@ class DecodeCache:
                              out.data_ptr(), scale, self.max_cap, self.step_ws.data_ptr(), self.step_ws_bytes,
                              _stream())
 
+    def step_layers(self, k_new: torch.Tensor, v_new: torch.Tensor, q: torch.Tensor, out: torch.Tensor,
+                    scale: float) -> None:
+        """The same decode step as L launches, one per layer (the loop of a
+        model that attends layer by layer): viscache_decode_step on each
+        layer's units, with the layer's slices of the pool tables, inputs and
+        outputs.  The launches are ordered on one stream, so they share one
+        step workspace."""
+        if not hasattr(self, "_layer_caches"):
+            per = self.B * self.Hkv
+            self.layer_shape = vc_decode_shape(self.B, 1, self.Hq, self.Hkv, self.d)
+            self._layer_caches = [
+                vc_cache(self.k_pool.data_ptr(), self.v_pool.data_ptr(), self.row_off[l * per:].data_ptr(),
+                         self.cap[l * per:].data_ptr(), self.len[l * per:].data_ptr()) for l in range(self.L)]
+            self.layer_caps = [max(self.caps_host[l * per:(l + 1) * per]) for l in range(self.L)]
+            nb = max(viscache_decode_step_workspace_bytes(self.layer_shape, c) for c in self.layer_caps)
+            self.layer_ws_bytes = max(nb, 256)
+            self.layer_ws = torch.zeros((self.layer_ws_bytes,), dtype=torch.uint8, device=self.k_pool.device)
+        for l in range(self.L):
+            viscache_decode_step(self.layer_shape, self._layer_caches[l], k_new[l].data_ptr(), v_new[l].data_ptr(),
+                                 q[l].data_ptr(), out[l].data_ptr(), scale, self.layer_caps[l],
+                                 self.layer_ws.data_ptr(), self.layer_ws_bytes, _stream())
+
     def quantize(self, nq) -> None:
         """Quantise every pool row to 4 bits (viscache_quantize_rows) and let
         unit u read its first nq[u] rows (rounded down to the 32-row tile)

@@ -14,13 +14,14 @@ def bf16_tensor(bits: np.ndarray, device) -> torch.Tensor:
 
 
 def upload_layers(w: Workload, layers, device, keep_host: bool = False, threads: int | None = None,
-                  prefill: bool = False):
+                  prefill: bool = False, host_only: bool = False):
     """Generate K, V (bf16 [rows, d]) and Q (fp32 [B, Hq, W, d]) for `layers`;
     with `prefill`, Q is the query of every prefill token (fp32
     [sum_b Hq*(n_b+W), d]) and 'KT' holds the text keys (bf16 [B, Hkv, W, d]).
 
     Returns (dev, host): dev maps 'K', 'V', 'Q' (and 'KT') to {layer: tensor};
-    host holds the numpy arrays when keep_host is set (else None)."""
+    host holds the numpy arrays when keep_host is set (else None).  With
+    host_only nothing is copied to a device (dev maps to empty dicts)."""
     roles = ("K", "V", "Q", "KT") if prefill else ("K", "V", "Q")
     dev = {r: {} for r in roles}
     host = {r: {} for r in roles} if keep_host else None
@@ -30,7 +31,8 @@ def upload_layers(w: Workload, layers, device, keep_host: bool = False, threads:
         if prefill:
             arrs["KT"] = w.ktext_layer(l)
         for r, a in arrs.items():
-            dev[r][l] = torch.from_numpy(a).to(device) if r == "Q" else bf16_tensor(a, device)
+            if not host_only:
+                dev[r][l] = torch.from_numpy(a).to(device) if r == "Q" else bf16_tensor(a, device)
             if keep_host:
                 host[r][l] = a
     return dev, host

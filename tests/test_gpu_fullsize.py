@@ -20,21 +20,12 @@ import os
 import numpy as np
 import pytest
 
-from tests.parity import TOL_BF16, TOL_FP32, check_sets, fused_error
+from tests.parity import SCORE_TOL, SCORE_TOL_CUT, SHARED_TOL, TOL_BF16, TOL_FP32, check_sets, fused_error, score_err
 
 pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 
-# Largest relative error of a GPU window score against the oracle's fp64
-# score, over scores above SCORE_FLOOR times the unit's largest score.  The
-# GPU takes bf16 x bf16 products into fp32 sums of d terms and fp32
-# exponentials (each within a few fp32 ulps), then sums G*W fp32
-# probabilities per key: about sqrt(d) + sqrt(G*W) roundings of 2^-24 each,
-# a few times 1e-6 in all.
-SCORE_TOL = 1e-5
-SCORE_FLOOR = 1e-20
-SHARED_TOL = 1e-5
 FUSE_SAMPLE_ROWS = 16
 
 
@@ -44,15 +35,6 @@ def _diag(rec):
         os.makedirs(d, exist_ok=True)
         with open(os.path.join(d, "parity_diag.jsonl"), "a") as f:
             f.write(json.dumps(rec) + "\n")
-
-
-def score_err(ref, got):
-    """Largest relative error over scores above SCORE_FLOOR x the largest."""
-    ref = np.asarray(ref, dtype=np.float64)
-    if ref.size == 0:
-        return 0.0
-    m = ref >= SCORE_FLOOR * ref.max()
-    return float((np.abs(np.asarray(got, dtype=np.float64)[m] - ref[m]) / ref[m]).max())
 
 
 @pytest.fixture(scope="module")
@@ -186,27 +168,31 @@ def _layer_head(fs, orc, all_rows=False, vfp32=False, drop_all=False):
 
     def one(u):
         ref = fs.S[u]
-        serr = score_err(ref, out.unit_scores(*u))
+        l, b, g = u
+        serr, scut = score_err(ref, out.unit_scores(*u), cut=out.ns[b * w.L + l])
         s, f = check_unit(orc, fs, out, *u, ref.astype(np.float32), tol, all_rows=all_rows)
-        return serr, s, f
+        return serr, scut, s, f
 
     res = orc.run_units(one, units)
     serr = max(r[0] for r in res)
+    scut = max(r[1] for r in res)
     rec = dict(workload=w.name, mode="layer_head", vfp32=vfp32, drop_all=drop_all, units=len(units),
-               swaps=sum(r[1] for r in res), fused_err=max(r[2] for r in res), score_rel_err=serr,
-               all_rows=all_rows)
+               swaps=sum(r[2] for r in res), fused_err=max(r[3] for r in res), score_rel_err=serr,
+               score_rel_err_cut=scut, all_rows=all_rows)
     print(f"[fullsize] {rec}", flush=True)
     _diag(rec)
     assert serr < SCORE_TOL, f"{w.name}: window score error {serr}"
+    assert scut < SCORE_TOL_CUT, f"{w.name}: window score error near the cuts {scut}"
     return out
 
 
 def _global(fs, orc):
     w = fs.w
     out = fs.run(1)
-    gerr = 0.0
+    gerr, gcut = 0.0, 0.0
     for b in range(w.B):
-        gerr = max(gerr, score_err(fs.gs[b], out.gs[fs.toff[b]:fs.toff[b + 1]]))
+        e, c = score_err(fs.gs[b], out.gs[fs.toff[b]:fs.toff[b + 1]], cut=out.ns[b * w.L])
+        gerr, gcut = max(gerr, e), max(gcut, c)
     # every layer's per-unit scores feed the shared one
     units_all = [(l, b, g) for l in range(w.L) for b in range(w.B) for g in range(w.Hkv)]
     serr = max(orc.run_units(lambda u: score_err(fs.S[u], out.unit_scores(*u)), units_all))
@@ -220,11 +206,12 @@ def _global(fs, orc):
                 k1 = out.unit(l, b, g)[0]
                 assert np.isin(k1, k0).all()
     rec = dict(workload=w.name, mode="global", units=len(units), swaps=sum(r[0] for r in res),
-               fused_err=max(r[1] for r in res), shared_rel_err=gerr, score_rel_err=serr)
+               fused_err=max(r[1] for r in res), shared_rel_err=gerr, shared_rel_err_cut=gcut, score_rel_err=serr)
     print(f"[fullsize] {rec}", flush=True)
     _diag(rec)
     assert serr < SCORE_TOL, f"{w.name}: window score error {serr}"
     assert gerr < SHARED_TOL, f"{w.name}: shared score error {gerr}"
+    assert gcut < SCORE_TOL_CUT, f"{w.name}: shared score error near the cuts {gcut}"
 
 
 # Cases in workload order, so each workload is generated and scored by the
