@@ -292,6 +292,32 @@ vc_status viscache_decode_step(const vc_decode_shape *shape, const vc_cache *cac
                                const void *v_new, const void *q, float *out, float scale,
                                int64_t max_rows, void *workspace, size_t workspace_bytes, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the
+ * library keeps one scratch array of VC_DECODE_NOALLOC_BYTES per device in
+ * its code object, held from load until the process ends, with room for the
+ * arrival counters of VC_DECODE_NOALLOC_UNITS units and the partial results
+ * of the launch's pieces. */
+#define VC_DECODE_NOALLOC_BYTES (16u << 20)
+#define VC_DECODE_NOALLOC_UNITS 65536
+
+/* Device, asynchronous.  viscache_decode_step without a workspace argument:
+ * the same append, attention and merge, the same results bit for bit, with
+ * the partial results and arrival counters in the library's scratch array of
+ * the current device (which must be the device of `stream` and of every
+ * pointer).  Allocates nothing: no hipMalloc, hipFree or allocating library
+ * call.  The first call on a device looks the array up and enqueues a clear
+ * of its counters on `stream`; every call leaves the counters at zero.
+ * Calls that overlap on one device race on the array: order them on one
+ * stream (calls on different devices are independent).  Every other
+ * argument and error as for viscache_decode_step, plus VC_ERR_WORKSPACE
+ * when L*B*Hkv > VC_DECODE_NOALLOC_UNITS or the partial results of the
+ * launch (16 (d + 2) floats per workgroup, workgroups as for
+ * viscache_decode_step_workspace_bytes) do not fit beside the counters. */
+vc_status viscache_decode_step_noalloc(const vc_decode_shape *shape, const vc_cache *cache, const void *k_new,
+                                       const void *v_new, const void *q, float *out, float scale,
+                                       int64_t max_rows, void *stream);
+
 /* ---- 4-bit cache rows ----------------------------------------------------
  * The quantisation experiments combine the pruned cache with 4-bit KV-cache
  * quantisation but do not define the quantiser.  The reading taken here: each

@@ -90,13 +90,15 @@ def lib() -> ctypes.CDLL:
                                            c_i64, c_vp, ctypes.c_size_t, c_vp]
         L.viscache_decode_step_q4.argtypes = [P(vc_decode_shape), P(vc_cache), P(vc_qcache), c_vp, c_vp, c_vp,
                                               c_vp, c_f32, c_i64, c_vp, ctypes.c_size_t, c_vp]
+        L.viscache_decode_step_noalloc.argtypes = [P(vc_decode_shape), P(vc_cache), c_vp, c_vp, c_vp, c_vp, c_f32,
+                                                   c_i64, c_vp]
         L.viscache_quantize_rows.argtypes = [c_i32, c_i64, c_vp, c_vp, c_vp, c_vp]
         L.viscache_strerror.argtypes = [c_i32]
         L.viscache_strerror.restype = ctypes.c_char_p
         for name in ("viscache_budget", "viscache_out_rows", "viscache_prune", "viscache_prune_score_offsets",
                      "viscache_prune_staged",
                      "viscache_append_kv", "viscache_decode_attn", "viscache_decode_step",
-                     "viscache_decode_step_q4", "viscache_quantize_rows"):
+                     "viscache_decode_step_q4", "viscache_decode_step_noalloc", "viscache_quantize_rows"):
             getattr(L, name).restype = c_i32
         _lib = L
     return _lib
@@ -248,6 +250,18 @@ def viscache_decode_step_q4(shape: vc_decode_shape, cache: vc_cache, qcache: vc_
            "viscache_decode_step_q4")
 
 
+VC_DECODE_NOALLOC_BYTES = 16 << 20
+VC_DECODE_NOALLOC_UNITS = 65536
+
+
+def viscache_decode_step_noalloc(shape: vc_decode_shape, cache: vc_cache, k_new: int, v_new: int, q: int, out: int,
+                                 scale: float, max_rows: int, stream: int) -> None:
+    """viscache_decode_step with the library's own per-device scratch (no
+    workspace argument; allocates nothing)."""
+    _check(lib().viscache_decode_step_noalloc(ctypes.byref(shape), ctypes.byref(cache), k_new, v_new, q, out, scale,
+                                              max_rows, stream), "viscache_decode_step_noalloc")
+
+
 def viscache_quantize_rows(d: int, rows: int, src: int, codes: int, meta: int, stream: int) -> None:
     _check(lib().viscache_quantize_rows(d, rows, src, codes, meta, stream), "viscache_quantize_rows")
 
@@ -260,4 +274,5 @@ EXPORTED = ("viscache_default_params", "viscache_budget", "viscache_out_rows",
             "viscache_prune_workspace_bytes", "viscache_prune_score_offsets", "viscache_prune",
             "viscache_prune_staged", "viscache_decode_workspace_bytes",
             "viscache_append_kv", "viscache_decode_attn", "viscache_decode_step_workspace_bytes",
-            "viscache_decode_step", "viscache_decode_step_q4", "viscache_quantize_rows", "viscache_strerror")
+            "viscache_decode_step", "viscache_decode_step_q4", "viscache_decode_step_noalloc",
+            "viscache_quantize_rows", "viscache_strerror")

@@ -17,6 +17,8 @@
 // A unit in one piece is normalised and written directly; the pieces of a
 // split unit leave partial (max, sum, O) results that are merged in row
 // order.
+#include <mutex>
+
 #include "vc_device.h"
 #include "vc_internal.h"
 
@@ -730,6 +732,49 @@ hipError_t launch_decode_step_q4(const DecodePlan &p, hipStream_t st) {
   else
     hipLaunchKernelGGL(k_decode_step_q4<64>, dim3(p.nwg), dim3(256), 0, st, p);
   return hipGetLastError();
+}
+
+// ---- scratch of the allocation-free decode step ---------------------------
+// One copy of this array per device, allocated when the code object is loaded
+// and held until the process ends: the arrival counters of split units at
+// the front (kNoAllocCounterBytes, zero between calls), the pieces' partial
+// results behind them.  Host code never passes the array's name to a
+// kernel (on the host it names a stand-in, not device memory); it uses the
+// device address hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) uint8_t scratch[kNoAllocBytes];
+
+namespace {
+__global__ __launch_bounds__(256) void k_clear_words(uint32_t *p, uint32_t n) {
+  for (uint32_t i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0u;
+}
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint8_t *g_scratch[kMaxDevices];
+}  // namespace
+
+hipError_t noalloc_scratch(uint8_t **out, hipStream_t st) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void *ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!ptr) return hipErrorInvalidSymbol;
+    // The counters start at zero (the array is zero when loaded; clear them
+    // anyway before the first call on this device uses them), and every
+    // call leaves them at zero.
+    hipLaunchKernelGGL(k_clear_words, dim3(kNoAllocCounterBytes / 4 / 256), dim3(256), 0, st,
+                       static_cast<uint32_t *>(ptr), (uint32_t)(kNoAllocCounterBytes / 4));
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    g_scratch[dev] = static_cast<uint8_t *>(ptr);
+  }
+  *out = g_scratch[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_decode(const DecodePlan &p, hipStream_t st) {

@@ -667,6 +667,36 @@ vc_status viscache_decode_step_q4(const vc_decode_shape *s, const vc_cache *c, c
   return VC_OK;
 }
 
+vc_status viscache_decode_step_noalloc(const vc_decode_shape *s, const vc_cache *c, const void *k_new,
+                                       const void *v_new, const void *q, float *out, float scale, int64_t max_rows,
+                                       void *stream) {
+  DecodePlan p;
+  const vc_status st = decode_plan(s, c, q, out, scale, max_rows, p);
+  if (st != VC_OK) return st;
+  if (!k_new || !v_new) return VC_ERR_ARG;
+  // The scratch holds the counters of at most kNoAllocUnits units and the
+  // partial results of the launch's pieces (as in decode_ws, without the
+  // two-call path's piece table).
+  const size_t o_bytes = align_up(sizeof(float) * (size_t)p.nwg * 16 * (size_t)p.d);
+  const size_t ml_bytes = align_up(sizeof(float2) * (size_t)p.nwg * 16);
+  if (p.units > kNoAllocUnits || kNoAllocCounterBytes + o_bytes + ml_bytes > kNoAllocBytes)
+    return VC_ERR_WORKSPACE;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  uint8_t *ws = nullptr;
+  if (noalloc_scratch(&ws, hs) != hipSuccess) return VC_ERR_HIP;
+  p.arrive = reinterpret_cast<uint32_t *>(ws);
+  p.part_o = reinterpret_cast<float *>(ws + kNoAllocCounterBytes);
+  p.part_ml = reinterpret_cast<float2 *>(ws + kNoAllocCounterBytes + o_bytes);
+  p.pinfo = nullptr;
+  p.k_pool_w = static_cast<uint16_t *>(c->k_pool);
+  p.v_pool_w = static_cast<uint16_t *>(c->v_pool);
+  p.len_w = c->len;
+  p.k_new = static_cast<const uint16_t *>(k_new);
+  p.v_new = static_cast<const uint16_t *>(v_new);
+  if (launch_decode_step(p, hs) != hipSuccess) return VC_ERR_HIP;
+  return VC_OK;
+}
+
 vc_status viscache_quantize_rows(int32_t d, int64_t rows, const void *src, void *codes, void *meta, void *stream) {
   if (d != 64 && d != 128) return VC_ERR_UNSUPPORTED;
   if (rows < 0) return VC_ERR_ARG;

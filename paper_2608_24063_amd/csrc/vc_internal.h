@@ -154,6 +154,17 @@ struct DecodePlan {
   const int32_t *nq;
 };
 
+// Scratch of the allocation-free decode step (viscache_decode_step_noalloc):
+// a file-scope device array of kNoAllocBytes per device.  The arrival
+// counters of at most kNoAllocUnits units sit at its front; the partial
+// results of the pieces fill the rest.
+constexpr size_t kNoAllocBytes = size_t(16) << 20;
+constexpr int32_t kNoAllocUnits = 65536;
+constexpr size_t kNoAllocCounterBytes = sizeof(uint32_t) * (size_t)kNoAllocUnits;
+// The current device's scratch (device address); the first call on a device
+// also enqueues, on `st`, the clear of the counters.
+hipError_t noalloc_scratch(uint8_t **out, hipStream_t st);
+
 hipError_t launch_append(int32_t units, int32_t d, uint16_t *k_pool, uint16_t *v_pool,
                          const int64_t *row_off, const int32_t *cap, int32_t *len,
                          const uint16_t *k_new, const uint16_t *v_new, hipStream_t st);

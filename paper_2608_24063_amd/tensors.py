@@ -7,7 +7,8 @@ import torch
 
 from . import (VC_PRUNE_EVENTS, VC_RANK_GLOBAL, make_params, make_prune_io, make_shape, prune_with_io, vc_cache,
                vc_decode_shape, vc_qcache, viscache_append_kv, viscache_budget, viscache_decode_attn,
-               viscache_decode_step, viscache_decode_step_q4, viscache_decode_step_workspace_bytes,
+               viscache_decode_step, viscache_decode_step_noalloc, viscache_decode_step_q4,
+               viscache_decode_step_workspace_bytes,
                viscache_decode_workspace_bytes, viscache_out_rows, viscache_prune_workspace_bytes,
                viscache_quantize_rows)
 
@@ -137,6 +138,13 @@ class DecodeCache:
         viscache_decode_step(self.shape, self.c, k_new.data_ptr(), v_new.data_ptr(), q.data_ptr(),
                              out.data_ptr(), scale, self.max_cap, self.step_ws.data_ptr(), self.step_ws_bytes,
                              _stream())
+
+    def step_noalloc(self, k_new: torch.Tensor, v_new: torch.Tensor, q: torch.Tensor, out: torch.Tensor,
+                     scale: float) -> None:
+        """step() through viscache_decode_step_noalloc: no workspace, the
+        library's own scratch."""
+        viscache_decode_step_noalloc(self.shape, self.c, k_new.data_ptr(), v_new.data_ptr(), q.data_ptr(),
+                                     out.data_ptr(), scale, self.max_cap, _stream())
 
     def step_layers(self, k_new: torch.Tensor, v_new: torch.Tensor, q: torch.Tensor, out: torch.Tensor,
                     scale: float) -> None:

@@ -129,6 +129,13 @@ static int run_case(int idx, const std::vector<double> &v) {
     CHECK(viscache_decode_step(&ds, &c, fake(905), fake(906), fake(907), static_cast<float *>(fake(908)),
                                0.088f, max_rows, fake(909), dws - 1, nullptr) == VC_ERR_WORKSPACE,
           "case %d: decode short workspace", idx);
+    // Allocation-free step: refused beyond its scratch, else it reaches the
+    // (stub) scratch lookup.
+    const bool fits = (int64_t)L * B * Hkv <= VC_DECODE_NOALLOC_UNITS &&
+                      dws <= (size_t)VC_DECODE_NOALLOC_BYTES - 4 * (size_t)VC_DECODE_NOALLOC_UNITS;
+    const vc_status na = viscache_decode_step_noalloc(&ds, &c, fake(905), fake(906), fake(907),
+                                                      static_cast<float *>(fake(908)), 0.088f, max_rows, nullptr);
+    CHECK(na == VC_ERR_HIP || (!fits && na == VC_ERR_WORKSPACE), "case %d: decode noalloc status %d", idx, (int)na);
   } else {
     CHECK(dws == 0, "case %d: decode group above 16 accepted", idx);
   }

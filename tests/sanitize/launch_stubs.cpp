@@ -43,6 +43,10 @@ hipError_t launch_append(int32_t, int32_t, uint16_t *, uint16_t *, const int64_t
 hipError_t launch_decode(const DecodePlan &p, hipStream_t) { return touch(&p, sizeof(p)); }
 hipError_t launch_decode_step(const DecodePlan &p, hipStream_t) { return touch(&p, sizeof(p)); }
 hipError_t launch_decode_step_q4(const DecodePlan &p, hipStream_t) { return touch(&p, sizeof(p)); }
+hipError_t noalloc_scratch(uint8_t **out, hipStream_t) {
+  *out = nullptr;
+  return hipErrorInvalidValue;
+}
 hipError_t launch_quant_rows(int32_t, int64_t, const uint16_t *, uint8_t *, float2 *, hipStream_t) {
   return hipErrorInvalidValue;
 }
