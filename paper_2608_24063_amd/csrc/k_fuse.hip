@@ -17,10 +17,14 @@
 //
 // Pipeline per workgroup: dropped-row indices are fetched four tiles ahead,
 // the rows themselves three tiles ahead into two register sets, and staged
-// into one of two LDS buffers one tile ahead; LDS operands of the matrix
-// products are read one k-step ahead.  The running row maximum is only
-// raised when a tile's logits exceed it by more than 2^kSlack, so most tiles
-// skip the cross-lane reduction and the rescale of the accumulators.
+// into one of two LDS buffers one tile ahead.  A tile is processed as two
+// halves of 32 dropped rows, which are the two k-steps of the second product:
+// the scores of the second half are issued before the softmax of the first,
+// and the first half's products with V_d^T before the softmax of the second,
+// so matrix and vector work can overlap.  The running row maximum is lazy: a
+// half's probabilities are taken against the maximum as it stands, and only
+// when their sum on some lane passes 2^64 (always on a job's first half) is
+// the maximum raised, the accumulators rescaled and the half redone.
 #include <type_traits>
 
 #include "vc_device.h"
@@ -31,9 +35,10 @@ namespace vc {
 namespace {
 
 constexpr float kNegInf = -__builtin_inff();
-// Probabilities are allowed to reach 2^kSlack before the running maximum is
-// raised (and the accumulators rescaled); fp32 has ample range for that.
-constexpr float kSlack = 8.f;
+// A half tile's probabilities against a stale maximum may sum to this much
+// before the maximum is raised: fp32 keeps the accumulators finite (at most
+// 2^15 dropped rows of values below 2^16 in magnitude).
+constexpr float kGrowLimit = 0x1p64f;
 
 // Staged dropped tile: rows of D bf16 at a pitch of D + 16 elements.  On
 // gfx950 (LDS serves 64 banks x 4 bytes per pass) this pitch keeps all three
@@ -56,6 +61,16 @@ __device__ __forceinline__ u32x2 lds_read_tr16(const uint16_t *p) {
   return __builtin_bit_cast(u32x2, v);
 }
 
+__device__ __forceinline__ uint32_t uni(uint32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+__device__ __forceinline__ uint64_t uni64(uint32_t lo, uint32_t hi) {
+  return (uint64_t)uni(lo) | ((uint64_t)uni(hi) << 32);
+}
+// Address `off` bytes past a wave-uniform base (32-bit offset arithmetic).
+template <typename T>
+__device__ __forceinline__ T *boff(uint64_t base, uint32_t off) {
+  return reinterpret_cast<T *>(base + off);
+}
+
 // Rows of one 64-row dropped tile between their global load and their LDS
 // store: thread t owns 16-byte chunk t % kCpr of rows t / kCpr + kRpp * it,
 // so every 16 lanes move whole rows (coalesced in HBM, conflict-free in LDS).
@@ -65,9 +80,9 @@ struct DropRegs {
   static constexpr int kRpp = 256 / kCpr;        // rows per pass of the block
   static constexpr int kIt = kDropTile / kRpp;   // rows per thread
   u32x4 v[kIt];
-  __device__ __forceinline__ void load(const uint16_t *V, const int (&row)[kIt], int chunk) {
+  __device__ __forceinline__ void load(uint64_t V, const int (&row)[kIt], int chunk) {
 #pragma unroll
-    for (int it = 0; it < kIt; ++it) v[it] = ld16(V + (int64_t)row[it] * D + chunk * 8);
+    for (int it = 0; it < kIt; ++it) v[it] = ld16(boff<const uint16_t>(V, (uint32_t)row[it] * (D * 2) + 16u * chunk));
   }
   __device__ __forceinline__ void store(uint16_t *vr, int row0, int chunk) const {
     constexpr int PR = kPitchRow<D>;
@@ -85,74 +100,65 @@ struct FuseState {
   float lsum[NB];      // this lane's share of the running denominator
 };
 
-// One 64-row dropped tile: S^T, online softmax, O^T.  MASK: the tile has
-// fewer than 64 valid rows (nd).
-template <int D, bool VFP32, bool MASK>
-__device__ __forceinline__ void fuse_tile(FuseState<D> &st, const uint16_t *vt, int nd, float tc, int lr,
-                                          int lg) {
-  constexpr int KS = D / 32, MB = D / 16, NB = 2, PR = kPitchRow<D>;
-
-  // S^T = V_d V_k^T for 64 dropped x 32 kept rows; A operands one k-step ahead.
-  f32x4 acc[NB][4];
-  bf16x8 a[2][4];
-  // k-step s, lane group lg: elements 32 s + 8 lg .. + 7 of the row.
-#pragma unroll
-  for (int db = 0; db < 4; ++db) a[0][db] = lds16(vt + (db * 16 + lr) * PR + 8 * lg);
+// S^T of one half tile (dropped rows 32 h .. 32 h + 31) for both kept
+// blocks; each operand read from LDS feeds two matrix instructions.
+template <int D>
+__device__ __forceinline__ void scores_half(const FuseState<D> &st, const uint16_t *vt, int h, int lr, int lg,
+                                            f32x4 (&acc)[2][2]) {
+  constexpr int KS = D / 32, PR = kPitchRow<D>;
 #pragma unroll
   for (int s = 0; s < KS; ++s) {
-    if (s + 1 < KS) {
+    bf16x8 a[2];
 #pragma unroll
-      for (int db = 0; db < 4; ++db)
-        a[(s + 1) & 1][db] = lds16(vt + (db * 16 + lr) * PR + 32 * (s + 1) + 8 * lg);
-    }
+    for (int d2 = 0; d2 < 2; ++d2) a[d2] = lds16(vt + (32 * h + 16 * d2 + lr) * PR + 32 * s + 8 * lg);
 #pragma unroll
-    for (int db = 0; db < 4; ++db)
+    for (int d2 = 0; d2 < 2; ++d2)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        acc[nb][db] = mfma_bf16(a[s & 1][db], st.bvk[nb][s], s == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : acc[nb][db]);
-    __builtin_amdgcn_sched_barrier(0);
+      for (int nb = 0; nb < 2; ++nb)
+        acc[nb][d2] = mfma_bf16(a[d2], st.bvk[nb][s], s == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : acc[nb][d2]);
   }
+}
 
-  // Transposed V_d operands of the first half of O^T, read while the
-  // softmax runs on the vector unit.
-  const int tr_row = 4 * lg + (lr >> 2), tr_col = 4 * (lr & 3);
-  const uint16_t *tbase = vt + tr_row * PR + tr_col;
-  constexpr int kPre = 4;
-  bf16x8 at[2 * MB];
+// Online softmax of one half tile: probabilities against the running max
+// (raised lazily), the denominators, and the bf16 B operands of O^T (with
+// VFP32, also the low parts).  MASK: rows at or past nd are not dropped rows.
+template <int D, bool VFP32, bool MASK>
+__device__ __forceinline__ void softmax_half(FuseState<D> &st, f32x4 (&acc)[2][2], int h, int nd, float tc, int lg,
+                                             bf16x8 (&ph)[2], bf16x8 (&pl)[2]) {
+  constexpr int MB = D / 16;
+  if (MASK) {
 #pragma unroll
-  for (int q = 0; q < kPre; ++q) {
-    const uint16_t *b0 = tbase + (32 * (q / MB)) * PR + 16 * (q % MB);
-    const u32x2 lo4 = lds_read_tr16(b0), hi4 = lds_read_tr16(b0 + 16 * PR);
-    at[q] = as_bf16x8(u32x4{lo4.x, lo4.y, hi4.x, hi4.y});
-  }
-  __builtin_amdgcn_sched_barrier(0);
-
-  // Online softmax over dropped rows.  The four lane groups of a kept row
-  // share one running max, raised (wave-uniformly) only when some logit
-  // exceeds it by more than 2^kSlack.
-  float tm[NB];
-  bool grow = false;
+    for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    if (MASK) {
-#pragma unroll
-      for (int db = 0; db < 4; ++db)
+      for (int d2 = 0; d2 < 2; ++d2)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          if (db * 16 + 4 * lg + i >= nd) acc[nb][db][i] = kNegInf;
-    }
-    float m = acc[nb][0][0];
-#pragma unroll
-    for (int db = 0; db < 4; ++db)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) m = fmaxf(m, acc[nb][db][i]);
-    tm[nb] = m * tc;
-    grow |= tm[nb] > st.mrow[nb] + kSlack;
+          if (32 * h + 16 * d2 + 4 * lg + i >= nd) acc[nb][d2][i] = kNegInf;
   }
-  if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+  float pr[2][2][4], part[2];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      float m = tm[nb];
+  for (int nb = 0; nb < 2; ++nb) {
+    part[nb] = 0.f;
+#pragma unroll
+    for (int d2 = 0; d2 < 2; ++d2)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        pr[nb][d2][i] = fast_exp2(fmaf(acc[nb][d2][i], tc, -st.mrow[nb]));
+        part[nb] += pr[nb][d2][i];
+      }
+  }
+  const bool grow = !(part[0] <= kGrowLimit && part[1] <= kGrowLimit);
+  if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+    // Raise each kept row's max to cover this half (the four lane groups of
+    // a row agree on it), rescale what is accumulated, redo the half.
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      float m = kNegInf;
+#pragma unroll
+      for (int d2 = 0; d2 < 2; ++d2)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) m = fmaxf(m, acc[nb][d2][i]);
+      m *= tc;
       m = fmaxf(m, shfl_xor(m, 16));
       m = fmaxf(m, shfl_xor(m, 32));
       const float mc = fmaxf(st.mrow[nb], m);
@@ -161,53 +167,64 @@ __device__ __forceinline__ void fuse_tile(FuseState<D> &st, const uint16_t *vt, 
       st.lsum[nb] *= alpha;
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) st.O[nb][mb] *= alpha;
+      part[nb] = 0.f;
+#pragma unroll
+      for (int d2 = 0; d2 < 2; ++d2)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          pr[nb][d2][i] = fast_exp2(fmaf(acc[nb][d2][i], tc, -mc));
+          part[nb] += pr[nb][d2][i];
+        }
     }
   }
-  bf16x8 bph[NB][2], bpl[NB][2];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    float pr[4][4];
-#pragma unroll
-    for (int db = 0; db < 4; ++db)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        pr[db][i] = fast_exp2(fmaf(acc[nb][db][i], tc, -st.mrow[nb]));
-        st.lsum[nb] += pr[db][i];
-      }
-#pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2) {
-      const float *p0 = pr[2 * t2], *p1 = pr[2 * t2 + 1];
-      const u32x4 hi = {pack_bf16(p0[0], p0[1]), pack_bf16(p0[2], p0[3]), pack_bf16(p1[0], p1[1]),
-                        pack_bf16(p1[2], p1[3])};
-      bph[nb][t2] = as_bf16x8(hi);
-      if (VFP32) {
-        const u32x4 lo = {pack_bf16(p0[0] - bf16_lo(hi.x), p0[1] - bf16_hi(hi.x)),
-                          pack_bf16(p0[2] - bf16_lo(hi.y), p0[3] - bf16_hi(hi.y)),
-                          pack_bf16(p1[0] - bf16_lo(hi.z), p1[1] - bf16_hi(hi.z)),
-                          pack_bf16(p1[2] - bf16_lo(hi.w), p1[3] - bf16_hi(hi.w))};
-        bpl[nb][t2] = as_bf16x8(lo);
-      }
+  for (int nb = 0; nb < 2; ++nb) {
+    st.lsum[nb] += part[nb];
+    const float *p0 = pr[nb][0], *p1 = pr[nb][1];
+    const u32x4 hi = {pack_bf16(p0[0], p0[1]), pack_bf16(p0[2], p0[3]), pack_bf16(p1[0], p1[1]),
+                      pack_bf16(p1[2], p1[3])};
+    ph[nb] = as_bf16x8(hi);
+    if (VFP32) {
+      const u32x4 lo = {pack_bf16(p0[0] - bf16_lo(hi.x), p0[1] - bf16_hi(hi.x)),
+                        pack_bf16(p0[2] - bf16_lo(hi.y), p0[3] - bf16_hi(hi.y)),
+                        pack_bf16(p1[0] - bf16_lo(hi.z), p1[1] - bf16_hi(hi.z)),
+                        pack_bf16(p1[2] - bf16_lo(hi.w), p1[3] - bf16_hi(hi.w))};
+      pl[nb] = as_bf16x8(lo);
     }
   }
-  __builtin_amdgcn_sched_barrier(0);
+}
 
-  // O^T += V_d^T P^T over two 32-row k-steps, operands kPre reads ahead.
+// O^T += V_d^T P^T for the k-step of one half tile: lane lr of lane group lg
+// reads dropped rows 32 h + 4 lg + (lr >> 2) and (+16), value columns
+// 16 mb + 4 (lr & 3) .. + 3, through the transposing read.
+template <int D, bool VFP32>
+__device__ __forceinline__ void values_half(FuseState<D> &st, const uint16_t *vt, int h, int lr, int lg,
+                                            const bf16x8 (&ph)[2], const bf16x8 (&pl)[2]) {
+  constexpr int MB = D / 16, PR = kPitchRow<D>;
+  const uint16_t *tb = vt + (32 * h + 4 * lg + (lr >> 2)) * PR + 4 * (lr & 3);
 #pragma unroll
-  for (int q = 0; q < 2 * MB; ++q) {
-    if (q + kPre < 2 * MB) {
-      const int qn = q + kPre;
-      const uint16_t *b0 = tbase + (32 * (qn / MB)) * PR + 16 * (qn % MB);
-      const u32x2 lo4 = lds_read_tr16(b0), hi4 = lds_read_tr16(b0 + 16 * PR);
-      at[qn] = as_bf16x8(u32x4{lo4.x, lo4.y, hi4.x, hi4.y});
-    }
-    const int t2 = q / MB, mb = q % MB;
+  for (int mb = 0; mb < MB; ++mb) {
+    const u32x2 lo4 = lds_read_tr16(tb + 16 * mb), hi4 = lds_read_tr16(tb + 16 * PR + 16 * mb);
+    const bf16x8 at = as_bf16x8(u32x4{lo4.x, lo4.y, hi4.x, hi4.y});
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      st.O[nb][mb] = mfma_bf16(at[q], bph[nb][t2], st.O[nb][mb]);
-      if (VFP32) st.O[nb][mb] = mfma_bf16(at[q], bpl[nb][t2], st.O[nb][mb]);
+    for (int nb = 0; nb < 2; ++nb) {
+      st.O[nb][mb] = mfma_bf16(at, ph[nb], st.O[nb][mb]);
+      if (VFP32) st.O[nb][mb] = mfma_bf16(at, pl[nb], st.O[nb][mb]);
     }
-    __builtin_amdgcn_sched_barrier(0);
   }
+}
+
+// One 64-row dropped tile (nd valid rows).
+template <int D, bool VFP32, bool MASK>
+__device__ __forceinline__ void fuse_tile(FuseState<D> &st, const uint16_t *vt, int nd, float tc, int lr, int lg) {
+  f32x4 accA[2][2], accB[2][2];
+  bf16x8 phA[2], plA[2], phB[2], plB[2];
+  scores_half<D>(st, vt, 0, lr, lg, accA);
+  scores_half<D>(st, vt, 1, lr, lg, accB);
+  softmax_half<D, VFP32, MASK>(st, accA, 0, nd, tc, lg, phA, plA);
+  values_half<D, VFP32>(st, vt, 0, lr, lg, phA, plA);
+  softmax_half<D, VFP32, MASK>(st, accB, 1, nd, tc, lg, phB, plB);
+  values_half<D, VFP32>(st, vt, 1, lr, lg, phB, plB);
 }
 
 // Workgroup = (fusion unit, 128 kept rows); wave w owns kept rows
@@ -216,22 +233,19 @@ __device__ __forceinline__ void fuse_tile(FuseState<D> &st, const uint16_t *vt, 
 template <int D>
 using DropTiles = uint16_t[2][kDropTile * kPitchRow<D>];
 
-// One fusion job: kept rows [128 tile, 128 tile + 128) of the unit of rank
-// `rank` in the fusion unit list.
-template <int D, bool VFP32>
-__device__ __forceinline__ void fuse_job(const PrunePlan &p, int rank, int tile, DropTiles<D> &vr) {
+// One fusion job: kept rows [128 tile, 128 tile + 128) of the unit whose
+// record is `rec`.  `next()` is called once the job's tiles are done (it
+// starts fetching the next job's record while this one blends and stores).
+template <int D, bool VFP32, typename Next>
+__device__ __forceinline__ void fuse_job(const PrunePlan &p, const u32x4 (&rec)[4], int tile, DropTiles<D> &vr,
+                                         Next &&next) {
   constexpr int KS = D / 32, MB = D / 16, NB = 2;
-  const u32x4 *rec = reinterpret_cast<const u32x4 *>(p.funit + rank);
-  const u32x4 r0 = ld16(rec), r1 = ld16(rec + 1), r2 = ld16(rec + 2), r3 = ld16(rec + 3);
-  auto ptr = [](uint32_t lo, uint32_t hi) { return (uint64_t)lo | ((uint64_t)hi << 32); };
-  const int k = (int)r3.x, r = (int)r3.y, n = (int)r3.z;
+  constexpr uint32_t kRowBytes = D * 2;
+  const uint64_t Kin = uni64(rec[0].x, rec[0].y), Vin = uni64(rec[0].z, rec[0].w);
+  const uint64_t Kout = uni64(rec[1].x, rec[1].y), Vout = uni64(rec[1].z, rec[1].w);
+  const uint64_t kept = uni64(rec[2].x, rec[2].y), drop = uni64(rec[2].z, rec[2].w);
+  const int k = (int)uni(rec[3].x), r = (int)uni(rec[3].y), n = (int)uni(rec[3].z);
   const int j0 = tile * kFuseRows;  // < k: the host lists only non-empty jobs
-  const uint16_t *Kin = reinterpret_cast<const uint16_t *>(ptr(r0.x, r0.y));
-  const uint16_t *Vin = reinterpret_cast<const uint16_t *>(ptr(r0.z, r0.w));
-  uint16_t *Kout = reinterpret_cast<uint16_t *>(ptr(r1.x, r1.y)) + (int64_t)j0 * D;
-  void *vout = reinterpret_cast<void *>(ptr(r1.z, r1.w));
-  const int32_t *kept = reinterpret_cast<const int32_t *>(ptr(r2.x, r2.y)) + j0;
-  const int32_t *drop = reinterpret_cast<const int32_t *>(ptr(r2.z, r2.w));
   const int nrows = min(kFuseRows, k - j0);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
@@ -239,7 +253,7 @@ __device__ __forceinline__ void fuse_job(const PrunePlan &p, int rank, int tile,
   // Token indices come from the selection kernel; clamping keeps every
   // gathered row inside the unit even if they were corrupted.
   auto clampi = [&](int v) { return min(max(v, 0), n - 1); };
-  auto kept_idx = [&](int row) { return ldg(kept + min(row, nrows - 1)); };
+  auto kept_idx = [&](int row) { return ldg(boff<const int32_t>(kept, 4u * (uint32_t)(j0 + min(row, nrows - 1)))); };
 
   // Every index this thread needs before the first tile, in one batch:
   // kept rows of its key-copy chunks and of its lanes' value operands, and
@@ -261,7 +275,8 @@ __device__ __forceinline__ void fuse_job(const PrunePlan &p, int rank, int tile,
   auto raw_idx = [&](int dt, int (&o)[kIt]) {
     const int base = min(dt, ntiles - 1) * kDropTile + row0;
 #pragma unroll
-    for (int it = 0; it < kIt; ++it) o[it] = ldg(drop + min(base + Regs::kRpp * it, r - 1));
+    for (int it = 0; it < kIt; ++it)
+      o[it] = ldg(boff<const int32_t>(drop, 4u * (uint32_t)min(base + Regs::kRpp * it, r - 1)));
   };
   auto clamp_rows = [&](const int (&in)[kIt], int (&o)[kIt]) {
 #pragma unroll
@@ -276,12 +291,15 @@ __device__ __forceinline__ void fuse_job(const PrunePlan &p, int rank, int tile,
   // Row loads: key copies, kept values, dropped tiles 0 and 1.
   u32x4 kc[kChunks];
 #pragma unroll
-  for (int i = 0; i < kChunks; ++i) kc[i] = ld16(Kin + (int64_t)clampi(kc_idx[i]) * D + ((tid + 256 * i) % kCpr) * 8);
+  for (int i = 0; i < kChunks; ++i)
+    kc[i] = ld16(boff<const uint16_t>(Kin, (uint32_t)clampi(kc_idx[i]) * kRowBytes + 16u * ((tid + 256 * i) % kCpr)));
   FuseState<D> st;
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
-    for (int s = 0; s < KS; ++s) st.bvk[nb][s] = as_bf16x8(ld16(Vin + (int64_t)clampi(kv_idx[nb]) * D + 32 * s + 8 * lg));
+    for (int s = 0; s < KS; ++s)
+      st.bvk[nb][s] = as_bf16x8(
+          ld16(boff<const uint16_t>(Vin, (uint32_t)clampi(kv_idx[nb]) * kRowBytes + 2u * (32 * s + 8 * lg))));
   }
   Regs set0, set1;
   int pend[kIt];  // raw indices of the next tile to load
@@ -297,7 +315,8 @@ __device__ __forceinline__ void fuse_job(const PrunePlan &p, int rank, int tile,
 #pragma unroll
   for (int i = 0; i < kChunks; ++i) {
     const int c = tid + 256 * i;
-    if (c / kCpr < nrows) st16(Kout + (int64_t)(c / kCpr) * D + (c % kCpr) * 8, kc[i]);
+    if (c / kCpr < nrows)
+      st16(boff<uint16_t>(Kout, (uint32_t)(j0 + c / kCpr) * kRowBytes + 16u * (c % kCpr)), kc[i]);
   }
   if (ntiles > 0) {
     set0.store(vr[0], row0, chunk);
@@ -323,7 +342,7 @@ __device__ __forceinline__ void fuse_job(const PrunePlan &p, int rank, int tile,
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) st.O[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
     // Running maxima are pre-multiplied by log2(e)/tau; the finite floor makes
-    // the first tile's rescale factor exp2(floor - max) = 0.
+    // the first half tile raise them (its probabilities overflow the limit).
     st.mrow[nb] = -1e30f;
     st.lsum[nb] = 0.f;
   }
@@ -363,6 +382,7 @@ __device__ __forceinline__ void fuse_job(const PrunePlan &p, int rank, int tile,
     const int nd = r - t * kDropTile;
     fuse_tile<D, VFP32, true>(st, vr[t & 1], nd, tc, lr, lg);
   }
+  next();
 
   const float mu = p.mu, omu = 1.f - p.mu;
 #pragma unroll
@@ -372,12 +392,12 @@ __device__ __forceinline__ void fuse_job(const PrunePlan &p, int rank, int tile,
     ls += shfl_xor(ls, 32);
     if (!kvalid[nb]) continue;
     const float inv = (r > 0 && ls > 0.f) ? 1.f / ls : 0.f;
-    const int64_t orow_j = j0 + w * 32 + nb * 16 + lr;
+    const uint32_t orow_j = (uint32_t)(j0 + w * 32 + nb * 16 + lr);
     // Kept values at this lane's output columns 16 mb + 4 lg + i (L2-hot).
-    const uint16_t *vrow = Vin + (int64_t)clampi(kv_idx[nb]) * D + 4 * lg;
+    const uint32_t vrow = (uint32_t)clampi(kv_idx[nb]) * kRowBytes + 8u * lg;
     u32x2 kvv[MB];
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) kvv[mb] = ld8(vrow + 16 * mb);
+    for (int mb = 0; mb < MB; ++mb) kvv[mb] = ld8(boff<const uint16_t>(Vin, vrow + 32u * mb));
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
       const uint32_t w0 = kvv[mb].x, w1 = kvv[mb].y;
@@ -385,28 +405,56 @@ __device__ __forceinline__ void fuse_job(const PrunePlan &p, int rank, int tile,
       float o[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) o[i] = (r > 0) ? mu * vk[i] + omu * (st.O[nb][mb][i] * inv) : vk[i];
-      const int64_t off = orow_j * D + mb * 16 + 4 * lg;
+      const uint32_t col = (uint32_t)(mb * 16 + 4 * lg);
       if (VFP32)
-        st16(reinterpret_cast<float *>(vout) + off,
+        st16(boff<float>(Vout, (orow_j * D + col) * 4u),
              u32x4{__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]), __float_as_uint(o[3])});
       else
-        st8(reinterpret_cast<uint16_t *>(vout) + off, u32x2{pack_bf16(o[0], o[1]), pack_bf16(o[2], o[3])});
+        st8(boff<uint16_t>(Vout, (orow_j * D + col) * 2u), u32x2{pack_bf16(o[0], o[1]), pack_bf16(o[2], o[3])});
     }
   }
 }
 
-// Persistent workgroups: block b walks the job list the host packed for it
-// (block b runs on XCD b % 8, which holds the L2 lines of its units).  Wave w
-// owns kept rows w*32 + nb*16 + [0, 16) of a job for nb = 0, 1, so every
-// operand read from LDS feeds two matrix instructions.
+// Persistent workgroups, the same number on every XCD: block b runs on XCD
+// x = b % 8 and works through that XCD's queue (its units' dropped rows stay
+// in that L2).  It starts on job b / 8 of the queue and then takes the next
+// untaken job each time it finishes one (one device-scope atomic per job,
+// issued while the finished job blends and stores), so the XCD's workgroups
+// stay busy until its queue is empty.  Every index is handed out once.
 template <int D, bool VFP32>
 __global__ __launch_bounds__(256, 2) void k_fuse(PrunePlan p) {
   __shared__ __attribute__((aligned(16))) DropTiles<D> vr;
-  const int j0 = ldg(p.fwoff + blockIdx.x), j1 = ldg(p.fwoff + blockIdx.x + 1);
-  for (int j = j0; j < j1; ++j) {
-    const int code = ldg(p.fwjob + j);
-    fuse_job<D, VFP32>(p, code >> 8, code & 255, vr);
-    __syncthreads();  // the next job restages the LDS tiles
+  __shared__ int s_code;
+  const int x = (int)(blockIdx.x % kXcds);
+  const int q0 = ldg(p.fwoff + x), qlen = ldg(p.fwoff + x + 1) - q0;
+  auto take = [&]() -> int {
+    __syncthreads();  // every thread has read the previous code
+    if (threadIdx.x == 0) {
+      const int i = __hip_atomic_fetch_add(p.fcnt + x, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      s_code = i < qlen ? ldg(p.fwjob + q0 + i) : -1;
+    }
+    __syncthreads();
+    return s_code;
+  };
+  auto fetch = [&](int code, u32x4 (&rec)[4]) {
+    const u32x4 *rp = reinterpret_cast<const u32x4 *>(p.funit + (code >> 8));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) rec[i] = ld16(rp + i);
+  };
+  const int first = (int)(blockIdx.x / kXcds);
+  int code = first < qlen ? ldg(p.fwjob + q0 + first) : -1;
+  u32x4 rec[4] = {};
+  if (code >= 0) fetch(code, rec);
+  while (code >= 0) {
+    int ncode = -1;
+    u32x4 nrec[4] = {};
+    fuse_job<D, VFP32>(p, rec, code & 255, vr, [&]() {
+      ncode = take();
+      if (ncode >= 0) fetch(ncode, nrec);
+    });
+    code = ncode;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) rec[i] = nrec[i];
   }
 }
 

@@ -27,12 +27,14 @@ struct Layout {
   int64_t Ntot;
   std::vector<int32_t> n, k, ns;       // n[B], k[B*L], ns[B*L]
   std::vector<int32_t> funit;          // fusion units, longest drop list first
-  std::vector<int32_t> fwoff, fwjob;   // fusion workgroup job lists (CSR): job = rank << 8 | tile
+  std::vector<int32_t> fwoff, fwjob;   // fusion job queues per XCD (CSR): job = rank << 8 | tile
+  std::vector<int32_t> fcnt0;          // jobs of each queue handed out at launch
+  int32_t nfwg = 0;                    // persistent fusion workgroups
   std::vector<int64_t> toff, orow, drow;
   // workspace regions (byte offsets)
   size_t off_plan, plan_bytes, off_qbf, off_part, off_S, off_gs, off_drop, total;
   // offsets inside the plan blob
-  size_t p_lp, p_nb, p_toff, p_kk, p_ns, p_orow, p_drow, p_funit, p_fwoff, p_fwjob;
+  size_t p_lp, p_nb, p_toff, p_kk, p_ns, p_orow, p_drow, p_funit, p_fwoff, p_fwjob, p_fcnt;
 };
 
 vc_status check_shape(const vc_shape *s) {
@@ -153,72 +155,52 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   };
   std::stable_sort(y.funit.begin(), y.funit.end(),
                    [&](int32_t a, int32_t c) { return drops(a) > drops(c); });
-  // Fusion jobs (unit, 128 kept rows) packed into persistent workgroups.  Unit
-  // of rank r goes to XCD r % 8 (all its jobs share its dropped rows in L2);
-  // inside an XCD, jobs are placed longest first on the least loaded of its
-  // workgroups (block b runs on XCD b % 8).  Cost of a job: its dropped
-  // tiles plus the fixed start-up of a job, in tile units.
+  // Fusion jobs (unit, 128 kept rows) in one queue per XCD.  Units are dealt
+  // to XCDs largest first, each to the XCD with the least work so far (all
+  // jobs of a unit share its dropped rows in that XCD's L2); each queue lists
+  // its jobs longest first.  Cost of a job: its dropped tiles plus a job's
+  // fixed start-up and wind-down, in tile units.  The persistent workgroups
+  // of an XCD (block b runs on XCD b % 8) start on the first jobs of its
+  // queue and take the rest one by one as they finish, so the work balances
+  // itself at run time.
   {
     constexpr int32_t kFuseSlots = 512;  // resident fusion workgroups (256 CUs x 2)
-    constexpr double kJobStart = 4.0;
-    struct Job { double cost; int32_t code; };
+    constexpr int64_t kJobStart = 4;
+    struct Job { int32_t cost; int32_t code; };
     std::vector<std::vector<Job>> xj(kXcdsHost);
-    {
-      std::vector<size_t> per(kXcdsHost, 0);
-      for (size_t rk = 0; rk < y.funit.size(); ++rk) {
-        const int32_t u = y.funit[rk];
-        const int32_t l = u / (y.Hkv * y.B), b = (u / y.Hkv) % y.B;
-        per[rk % kXcdsHost] += (size_t)((y.k[(size_t)b * y.L + l] + kFuseRows - 1) / kFuseRows);
-      }
-      for (int32_t x = 0; x < kXcdsHost; ++x) xj[x].reserve(per[x]);
-    }
+    std::vector<int64_t> xload(kXcdsHost, 0);
     int64_t njobs = 0;
     for (size_t rk = 0; rk < y.funit.size(); ++rk) {
       const int32_t u = y.funit[rk];
       const int32_t l = u / (y.Hkv * y.B), b = (u / y.Hkv) % y.B;
       const int32_t kk = y.k[(size_t)b * y.L + l];
       const int32_t rr = y.ns[(size_t)b * y.L + l] - kk;
-      const double cost = kJobStart + (double)((rr + kDropTile - 1) / kDropTile);
-      for (int32_t t = 0; t * kFuseRows < kk; ++t) {
-        xj[rk % kXcdsHost].push_back({cost, (int32_t)(rk << 8) | t});
-        ++njobs;
-      }
+      const int32_t cost = (rr + kDropTile - 1) / kDropTile;
+      const int32_t nj = (kk + kFuseRows - 1) / kFuseRows;
+      const int32_t x = (int32_t)(std::min_element(xload.begin(), xload.end()) - xload.begin());
+      xload[x] += (int64_t)nj * (kJobStart + cost);
+      for (int32_t t = 0; t < nj; ++t) xj[x].push_back({cost, (int32_t)(rk << 8) | t});
+      njobs += nj;
     }
-    const int32_t per_xcd = (int32_t)std::max<int64_t>(
-        1, std::min<int64_t>(kFuseSlots / kXcdsHost, (njobs + kXcdsHost - 1) / kXcdsHost));
-    const int32_t nwg = per_xcd * kXcdsHost;
-    // Job j of XCD x (in placement order) goes to workgroup x + 8*slot[x][j]:
-    // the least loaded slot, the lowest index among equal loads (a binary
-    // heap on (load, slot)).  Then a counting pass lays the lists out in CSR
-    // form, each list in placement order.
-    std::vector<int32_t> wg_of;  // per job, XCD by XCD in placement order
-    wg_of.reserve((size_t)njobs);
-    std::vector<std::pair<double, int32_t>> heap((size_t)per_xcd);
-    auto later = [](const std::pair<double, int32_t> &a, const std::pair<double, int32_t> &c) {
-      return a.first != c.first ? a.first > c.first : a.second > c.second;
-    };
+    y.fwoff.assign(kXcdsHost + 1, 0);
+    y.fwjob.clear();
+    y.fwjob.reserve((size_t)njobs);
+    size_t longest = 0;
     for (int32_t x = 0; x < kXcdsHost; ++x) {
       auto &jl = xj[x];
       // Units come longest drop list first, so the jobs usually are in order.
       auto longer = [](const Job &a, const Job &c) { return a.cost > c.cost; };
       if (!std::is_sorted(jl.begin(), jl.end(), longer)) std::stable_sort(jl.begin(), jl.end(), longer);
-      for (int32_t i = 0; i < per_xcd; ++i) heap[i] = {0.0, i};
-      for (const Job &j : jl) {
-        std::pop_heap(heap.begin(), heap.end(), later);
-        auto &top = heap.back();
-        wg_of.push_back(x + kXcdsHost * top.second);
-        top.first += j.cost;
-        std::push_heap(heap.begin(), heap.end(), later);
-      }
+      for (const Job &j : jl) y.fwjob.push_back(j.code);
+      y.fwoff[(size_t)x + 1] = (int32_t)y.fwjob.size();
+      longest = std::max(longest, jl.size());
     }
-    y.fwoff.assign((size_t)nwg + 1, 0);
-    for (int32_t w : wg_of) ++y.fwoff[(size_t)w + 1];
-    for (int32_t w = 0; w < nwg; ++w) y.fwoff[(size_t)w + 1] += y.fwoff[(size_t)w];
-    y.fwjob.assign((size_t)njobs, 0);
-    std::vector<int32_t> fill(y.fwoff.begin(), y.fwoff.end() - 1);
-    size_t idx = 0;
+    y.nfwg = (int32_t)std::min<int64_t>(kFuseSlots / kXcdsHost, (int64_t)longest) * kXcdsHost;
+    // Jobs already handed out per queue: each of the XCD's workgroups starts
+    // on one of the first jobs.
+    y.fcnt0.assign(kXcdsHost, 0);
     for (int32_t x = 0; x < kXcdsHost; ++x)
-      for (const Job &j : xj[x]) y.fwjob[(size_t)fill[(size_t)wg_of[idx++]]++] = j.code;
+      y.fcnt0[(size_t)x] = std::min<int32_t>(y.nfwg / kXcdsHost, (int32_t)xj[x].size());
   }
 
   // Plan blob.
@@ -236,6 +218,7 @@ vc_status make_layout(const vc_shape *s, const vc_params *p, Layout &y) {
   o = (o + 15) & ~size_t(15);
   y.p_funit = o; o += sizeof(FuseUnit) * y.funit.size();
   y.p_fwoff = o; o += sizeof(int32_t) * y.fwoff.size();
+  y.p_fcnt = o; o += sizeof(int32_t) * kXcdsHost;  // queue counters, reset by every plan upload
   y.p_fwjob = o; o += sizeof(int32_t) * y.fwjob.size();
   o = (o + 7) & ~size_t(7);
   y.plan_bytes = o;
@@ -419,6 +402,7 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   std::memcpy(blob.data() + y.p_kk, y.k.data(), sizeof(int32_t) * y.k.size());
   std::memcpy(blob.data() + y.p_ns, y.ns.data(), sizeof(int32_t) * y.ns.size());
   std::memcpy(blob.data() + y.p_fwoff, y.fwoff.data(), sizeof(int32_t) * y.fwoff.size());
+  std::memcpy(blob.data() + y.p_fcnt, y.fcnt0.data(), sizeof(int32_t) * y.fcnt0.size());
   if (!y.fwjob.empty()) std::memcpy(blob.data() + y.p_fwjob, y.fwjob.data(), sizeof(int32_t) * y.fwjob.size());
   {
     // Fusion unit records: absolute row addresses, so the fusion kernel
@@ -453,7 +437,7 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   pl.nqg = y.nqg; pl.nks = y.nks; pl.ncol = y.ncol; pl.nmax = y.nmax;
   pl.pwg = y.pwg;
   pl.nfunits = (int32_t)y.funit.size();
-  pl.nfwg = (int32_t)y.fwoff.size() - 1;
+  pl.nfwg = y.nfwg;
   pl.sc = (float)(1.4426950408889634 / std::sqrt((double)y.d));
   pl.tc = (float)(1.4426950408889634 / (double)params->tau);
   pl.mu = params->mu;
@@ -472,6 +456,7 @@ vc_status viscache_prune_staged(const vc_shape *shape, const vc_params *params, 
   pl.funit = reinterpret_cast<const FuseUnit *>(pb + y.p_funit);
   pl.fwoff = reinterpret_cast<const int32_t *>(pb + y.p_fwoff);
   pl.fwjob = reinterpret_cast<const int32_t *>(pb + y.p_fwjob);
+  pl.fcnt = reinterpret_cast<int32_t *>(pb + y.p_fcnt);
   pl.qbf = reinterpret_cast<uint16_t *>(ws + y.off_qbf);
   pl.part = reinterpret_cast<float2 *>(ws + y.off_part);
   pl.pcol = reinterpret_cast<float *>(ws + y.off_part);

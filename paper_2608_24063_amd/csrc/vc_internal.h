@@ -56,7 +56,7 @@ struct PrunePlan {
   int32_t nqg, nks;   // stats grid: query groups x key splits per unit
   int32_t ncol;       // column-sum chunks per unit (max over sequences)
   int32_t nfunits;    // units with kept rows
-  int32_t nfwg;       // fusion workgroups (persistent; each walks its job list)
+  int32_t nfwg;       // fusion workgroups (persistent; a multiple of 8, the same number per XCD)
   int32_t nmax;       // max n_b
   int32_t pwg;        // prefill: workgroups per unit (each owns every pwg-th 256-row group)
   float sc;           // log2(e) / sqrt(d)
@@ -72,8 +72,9 @@ struct PrunePlan {
   const int64_t *orow;  // [L*(B+1)] output row offsets per layer
   const int64_t *drow;  // [L*(B+1)] dropped-row offsets per layer
   const FuseUnit *funit; // [nfunits] fusion units, most dropped rows first
-  const int32_t *fwoff;  // [nfwg+1] job list offsets per fusion workgroup
-  const int32_t *fwjob;  // fusion jobs: unit rank << 8 | 128-row tile
+  const int32_t *fwoff;  // [9] job queue offsets per XCD
+  const int32_t *fwjob;  // fusion jobs: unit rank << 8 | 128-row tile, each queue longest first
+  int32_t *fcnt;         // [8] jobs handed out per queue (reset by every plan upload)
   uint16_t *qbf;        // [Ls][B][Hq][W][d] window queries in bf16
   float2 *part;         // [U][nks][R] partial row statistics (max*sc, sum)
   float *pcol;          // prefill: [U][pwg][nmax] column partials of each workgroup
