@@ -361,8 +361,10 @@ def decode_latency(w, pc, dev, steps, flush_buf, torch, sg):
     """Per-step latency of append + attention over all layers, on the full,
     pruned and empty-visual caches and on the pruned cache with its kept rows
     in 4 bits (whole 32-row tiles; text and generated rows in bf16), in one
-    launch per step; and the full, pruned and empty caches again with one
-    launch per layer (a model's layer loop)."""
+    launch per step over a piece table built once per cache
+    (viscache_decode_step_planned); the same four with the cut made on the
+    device in every step (viscache_decode_step / _q4); and the full, pruned
+    and empty caches with one launch per layer (a model's layer loop)."""
     from paper_2608_24063_amd.tensors import DecodeCache
     from synthgen.device import bf16_tensor
     L, B, Hkv, d = w.L, w.B, w.Hkv, w.d
@@ -377,8 +379,9 @@ def decode_latency(w, pc, dev, steps, flush_buf, torch, sg):
     toff = [0]
     for x in n:
         toff.append(toff[-1] + x)
-    for variant in ("full", "pruned", "empty", "pruned_q4", "full_layers", "pruned_layers", "empty_layers"):
-        base = variant.replace("_layers", "")
+    for variant in ("full", "pruned", "empty", "pruned_q4", "full_cut", "pruned_cut", "empty_cut", "pruned_q4_cut",
+                    "full_layers", "pruned_layers", "empty_layers"):
+        base = variant.replace("_layers", "").replace("_cut", "")
         vis = []
         for l in range(L):
             for b in range(B):
@@ -410,11 +413,18 @@ def decode_latency(w, pc, dev, steps, flush_buf, torch, sg):
                     lens.append(v + w.W)
         c.len.copy_(torch.tensor(lens, dtype=torch.int32))
         rows0 = sum(lens)
-        nq = [v // 32 * 32 for v in vis] if variant == "pruned_q4" else [0] * len(vis)
-        step = c.step_layers if variant.endswith("_layers") else c.step
-        if variant == "pruned_q4":
+        nq = [v // 32 * 32 for v in vis] if base == "pruned_q4" else [0] * len(vis)
+        if base == "pruned_q4":
             c.quantize(nq)
-            step = c.step_q4
+        if variant.endswith("_layers"):
+            step = c.step_layers
+        elif variant.endswith("_cut"):
+            step = c.step_q4 if base == "pruned_q4" else c.step
+        else:
+            c.plan()  # once per cache, outside the timed steps
+
+            def step(k, v, qq, o, sc, _c=c, _q4=(base == "pruned_q4")):
+                _c.step_planned(k, v, qq, o, sc, q4=_q4)
         ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
               for _ in range(steps)]
         torch.cuda.synchronize()
@@ -442,6 +452,8 @@ def decode_latency(w, pc, dev, steps, flush_buf, torch, sg):
     rho, bound = target(full, pr, em)
     fl, pl, el = results["full_layers"], results["pruned_layers"], results["empty_layers"]
     _, bound_l = target(fl, pl, el)
+    fc, pcut, ec, pqc = results["full_cut"], results["pruned_cut"], results["empty_cut"], results["pruned_q4_cut"]
+    _, bound_c = target(fc, pcut, ec)
     return dict(steps=steps, full_us=full["median_us"], pruned_us=pr["median_us"], empty_us=em["median_us"],
                 full_mean_us=full["mean_us"], pruned_mean_us=pr["mean_us"],
                 speedup=full["median_us"] / pr["median_us"], rho=rho,
@@ -452,6 +464,9 @@ def decode_latency(w, pc, dev, steps, flush_buf, torch, sg):
                 speedup_q4=full["median_us"] / pq["median_us"],
                 q4_bytes_ratio=pq["bytes_per_step"] / pr["bytes_per_step"],
                 pruned_q4_hbm_gbs=pq["bytes_per_step"] / (pq["median_us"] * 1e3),
+                device_cut=dict(full_us=fc["median_us"], pruned_us=pcut["median_us"], empty_us=ec["median_us"],
+                                pruned_q4_us=pqc["median_us"], speedup=fc["median_us"] / pcut["median_us"],
+                                target_speedup=fc["median_us"] / bound_c, meets_target=pcut["median_us"] <= bound_c),
                 per_layer_launch=dict(launches_per_step=L, full_us=fl["median_us"], pruned_us=pl["median_us"],
                                       empty_us=el["median_us"], speedup=fl["median_us"] / pl["median_us"],
                                       target_speedup=fl["median_us"] / bound_l,

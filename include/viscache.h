@@ -363,6 +363,53 @@ vc_status viscache_decode_step_q4(const vc_decode_shape *shape, const vc_cache *
                                   const void *k_new, const void *v_new, const void *q, float *out, float scale,
                                   int64_t max_rows, void *workspace, size_t workspace_bytes, void *stream);
 
+/* ---- decode with a piece table built once per cache ----------------------
+ * The decode calls above cut every unit's rows into workgroup pieces on the
+ * device, in every step, from the capacities.  Capacities do not change
+ * between steps, so the cut can be made once, on the host, from host copies
+ * of cap and row_off (Sec. 2, decoding: the cache of each step is the
+ * previous one plus one row). */
+
+/* Host only.  Bytes of the piece table for decode steps of this shape and row
+ * bound (a 32-byte header and 32 bytes per workgroup of the launch); 0 where
+ * viscache_decode_step_workspace_bytes is 0. */
+size_t viscache_decode_plan_bytes(const vc_decode_shape *shape, int64_t max_rows);
+
+/* Host only.  Builds the piece table of the caches whose capacities and first
+ * pool rows are cap and row_off (HOST arrays of L*B*Hkv entries, the same
+ * values as the vc_cache's device arrays) into `plan` (HOST, 4-byte aligned,
+ * at least viscache_decode_plan_bytes bytes), for steps with this max_rows.
+ * The caller copies the table to device memory and passes it to
+ * viscache_decode_step_planned.  Each unit's min(cap, max_rows) rows are cut
+ * into whole 32-row tiles; a workgroup's piece is shared by its four waves in
+ * runs of consecutive tiles, and the table takes the smallest per-wave share
+ * (at least two tiles) for which the pieces fit the launch.  VC_ERR_ARG for a
+ * null pointer, a negative capacity or offset, negative max_rows, or units
+ * whose blocks overlap; VC_ERR_UNSUPPORTED for a capacity above 2^31 - 65 or
+ * a size viscache_decode_plan_bytes refuses; VC_ERR_WORKSPACE if plan_bytes
+ * is too small.  The table stays valid while cap and row_off do not change;
+ * after a change, build it again (a stale table attends the wrong rows and
+ * may read outside the caches' blocks). */
+vc_status viscache_decode_plan(const vc_decode_shape *shape, const int32_t *cap, const int64_t *row_off,
+                               int64_t max_rows, void *plan, size_t plan_bytes);
+
+/* Device, asynchronous.  viscache_decode_step (qcache NULL) or
+ * viscache_decode_step_q4 (qcache non-NULL, as there) over the cut of a piece
+ * table: the same append, attention and merge, equal to those calls up to
+ * rounding (the pieces differ).  plan: DEVICE copy of a table from
+ * viscache_decode_plan for this cache, shape and max_rows, 16-byte aligned,
+ * plan_bytes at least viscache_decode_plan_bytes; a table built for another
+ * shape or max_rows fills `out` with NaN.  The workspace is that of
+ * viscache_decode_step (viscache_decode_step_workspace_bytes, zero-filled
+ * before its first use, left at zero by every call); calls sharing it must be
+ * ordered on one stream.  Every other argument and error as for
+ * viscache_decode_step and viscache_decode_step_q4, plus VC_ERR_ARG for a
+ * null or misaligned plan or a too small plan_bytes. */
+vc_status viscache_decode_step_planned(const vc_decode_shape *shape, const vc_cache *cache, const vc_qcache *qcache,
+                                       const void *plan, size_t plan_bytes, const void *k_new, const void *v_new,
+                                       const void *q, float *out, float scale, int64_t max_rows, void *workspace,
+                                       size_t workspace_bytes, void *stream);
+
 /* Static text for a status code. */
 const char *viscache_strerror(vc_status s);
 

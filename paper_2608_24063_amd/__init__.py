@@ -92,13 +92,20 @@ def lib() -> ctypes.CDLL:
                                               c_vp, c_f32, c_i64, c_vp, ctypes.c_size_t, c_vp]
         L.viscache_decode_step_noalloc.argtypes = [P(vc_decode_shape), P(vc_cache), c_vp, c_vp, c_vp, c_vp, c_f32,
                                                    c_i64, c_vp]
+        L.viscache_decode_plan_bytes.argtypes = [P(vc_decode_shape), c_i64]
+        L.viscache_decode_plan_bytes.restype = ctypes.c_size_t
+        L.viscache_decode_plan.argtypes = [P(vc_decode_shape), P(c_i32), P(c_i64), c_i64, c_vp, ctypes.c_size_t]
+        L.viscache_decode_step_planned.argtypes = [P(vc_decode_shape), P(vc_cache), P(vc_qcache), c_vp,
+                                                   ctypes.c_size_t, c_vp, c_vp, c_vp, c_vp, c_f32, c_i64, c_vp,
+                                                   ctypes.c_size_t, c_vp]
         L.viscache_quantize_rows.argtypes = [c_i32, c_i64, c_vp, c_vp, c_vp, c_vp]
         L.viscache_strerror.argtypes = [c_i32]
         L.viscache_strerror.restype = ctypes.c_char_p
         for name in ("viscache_budget", "viscache_out_rows", "viscache_prune", "viscache_prune_score_offsets",
                      "viscache_prune_staged",
                      "viscache_append_kv", "viscache_decode_attn", "viscache_decode_step",
-                     "viscache_decode_step_q4", "viscache_decode_step_noalloc", "viscache_quantize_rows"):
+                     "viscache_decode_step_q4", "viscache_decode_step_noalloc", "viscache_decode_plan",
+                     "viscache_decode_step_planned", "viscache_quantize_rows"):
             getattr(L, name).restype = c_i32
         _lib = L
     return _lib
@@ -262,6 +269,34 @@ def viscache_decode_step_noalloc(shape: vc_decode_shape, cache: vc_cache, k_new:
                                               max_rows, stream), "viscache_decode_step_noalloc")
 
 
+def viscache_decode_plan_bytes(shape: vc_decode_shape, max_rows: int) -> int:
+    return int(lib().viscache_decode_plan_bytes(ctypes.byref(shape), max_rows))
+
+
+def viscache_decode_plan(shape: vc_decode_shape, cap, row_off, max_rows: int) -> bytes:
+    """The piece table of caches with capacities `cap` and first pool rows
+    `row_off` (host sequences), built on the host; returns its bytes."""
+    n = len(cap)
+    cap_a = (c_i32 * n)(*[int(x) for x in cap])
+    off_a = (c_i64 * n)(*[int(x) for x in row_off])
+    nbytes = viscache_decode_plan_bytes(shape, max_rows)
+    buf = (ctypes.c_int32 * max(nbytes // 4, 1))()
+    _check(lib().viscache_decode_plan(ctypes.byref(shape), cap_a, off_a, max_rows, ctypes.addressof(buf), nbytes),
+           "viscache_decode_plan")
+    return bytes(buf)[:nbytes]
+
+
+def viscache_decode_step_planned(shape: vc_decode_shape, cache: vc_cache, qcache, plan: int, plan_bytes: int,
+                                 k_new: int, v_new: int, q: int, out: int, scale: float, max_rows: int,
+                                 workspace: int, workspace_bytes: int, stream: int) -> None:
+    """viscache_decode_step (qcache None) or viscache_decode_step_q4 over a
+    device copy of a piece table."""
+    qc = ctypes.byref(qcache) if qcache is not None else None
+    _check(lib().viscache_decode_step_planned(ctypes.byref(shape), ctypes.byref(cache), qc, plan, plan_bytes, k_new,
+                                              v_new, q, out, scale, max_rows, workspace, workspace_bytes, stream),
+           "viscache_decode_step_planned")
+
+
 def viscache_quantize_rows(d: int, rows: int, src: int, codes: int, meta: int, stream: int) -> None:
     _check(lib().viscache_quantize_rows(d, rows, src, codes, meta, stream), "viscache_quantize_rows")
 
@@ -275,4 +310,5 @@ EXPORTED = ("viscache_default_params", "viscache_budget", "viscache_out_rows",
             "viscache_prune_staged", "viscache_decode_workspace_bytes",
             "viscache_append_kv", "viscache_decode_attn", "viscache_decode_step_workspace_bytes",
             "viscache_decode_step", "viscache_decode_step_q4", "viscache_decode_step_noalloc",
+            "viscache_decode_plan_bytes", "viscache_decode_plan", "viscache_decode_step_planned",
             "viscache_quantize_rows", "viscache_strerror")

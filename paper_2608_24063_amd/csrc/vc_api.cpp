@@ -682,6 +682,65 @@ vc_status viscache_decode_step_noalloc(const vc_decode_shape *s, const vc_cache 
   return VC_OK;
 }
 
+size_t viscache_decode_plan_bytes(const vc_decode_shape *s, int64_t max_rows) {
+  if (check_decode(s) != VC_OK || max_rows < 0) return 0;
+  const int64_t units = (int64_t)s->L * s->B * s->Hkv;
+  const int32_t nwg = decode_grid(units, max_rows);
+  if (nwg < 1) return 0;
+  return decode_plan_table_bytes(nwg);
+}
+
+vc_status viscache_decode_plan(const vc_decode_shape *s, const int32_t *cap, const int64_t *row_off,
+                               int64_t max_rows, void *plan, size_t plan_bytes) {
+  vc_status st = check_decode(s);
+  if (st != VC_OK) return st;
+  if (!cap || !row_off || !plan || max_rows < 0) return VC_ERR_ARG;
+  if (reinterpret_cast<uintptr_t>(plan) % alignof(int32_t) != 0) return VC_ERR_ARG;
+  const size_t need = viscache_decode_plan_bytes(s, max_rows);
+  if (need == 0) return VC_ERR_UNSUPPORTED;
+  if (plan_bytes < need) return VC_ERR_WORKSPACE;
+  const int64_t units = (int64_t)s->L * s->B * s->Hkv;
+  return (vc_status)decode_plan_build((int32_t)units, cap, row_off, max_rows, decode_grid(units, max_rows), s->d,
+                                      static_cast<int32_t *>(plan));
+}
+
+vc_status viscache_decode_step_planned(const vc_decode_shape *s, const vc_cache *c, const vc_qcache *qc,
+                                       const void *plan, size_t plan_bytes, const void *k_new, const void *v_new,
+                                       const void *q, float *out, float scale, int64_t max_rows, void *workspace,
+                                       size_t workspace_bytes, void *stream) {
+  DecodePlan p;
+  const vc_status st = decode_plan(s, c, q, out, scale, max_rows, p);
+  if (st != VC_OK) return st;
+  if (!k_new || !v_new || !plan) return VC_ERR_ARG;
+  if (reinterpret_cast<uintptr_t>(plan) % 16 != 0 || plan_bytes < decode_plan_table_bytes(p.nwg)) return VC_ERR_ARG;
+  if (qc) {
+    if (!qc->k_codes || !qc->k_meta || !qc->v_codes || !qc->v_meta || !qc->qrow_off || !qc->nq) return VC_ERR_ARG;
+    if ((reinterpret_cast<uintptr_t>(qc->k_codes) | reinterpret_cast<uintptr_t>(qc->v_codes)) % 4 != 0 ||
+        (reinterpret_cast<uintptr_t>(qc->k_meta) | reinterpret_cast<uintptr_t>(qc->v_meta)) % 8 != 0)
+      return VC_ERR_ARG;
+  }
+  const size_t need = viscache_decode_step_workspace_bytes(s, max_rows);
+  if (!workspace || workspace_bytes < need) return VC_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return VC_ERR_WORKSPACE;
+  decode_bind_ws(p, static_cast<uint8_t *>(workspace));
+  p.k_pool_w = static_cast<uint16_t *>(c->k_pool);
+  p.v_pool_w = static_cast<uint16_t *>(c->v_pool);
+  p.len_w = c->len;
+  p.k_new = static_cast<const uint16_t *>(k_new);
+  p.v_new = static_cast<const uint16_t *>(v_new);
+  p.plan = static_cast<const int32_t *>(plan);
+  if (qc) {
+    p.qk = static_cast<const uint8_t *>(qc->k_codes);
+    p.qv = static_cast<const uint8_t *>(qc->v_codes);
+    p.qkm = static_cast<const float2 *>(qc->k_meta);
+    p.qvm = static_cast<const float2 *>(qc->v_meta);
+    p.qoff = qc->qrow_off;
+    p.nq = qc->nq;
+  }
+  if (launch_decode_planned(p, qc != nullptr, static_cast<hipStream_t>(stream)) != hipSuccess) return VC_ERR_HIP;
+  return VC_OK;
+}
+
 vc_status viscache_quantize_rows(int32_t d, int64_t rows, const void *src, void *codes, void *meta, void *stream) {
   if (d != 64 && d != 128) return VC_ERR_UNSUPPORTED;
   if (rows < 0) return VC_ERR_ARG;

@@ -98,6 +98,23 @@ __device__ __forceinline__ T shfl_xor(T v, int mask) {
   return __shfl_xor(v, mask, 64);
 }
 
+// Exchanges between lanes i and i ^ 16 / i ^ 32 that need no lane-index
+// register (the generic shuffle keeps per-lane indices live across loops):
+// an LDS swizzle swaps the 16-lane groups of each 32-lane half, and gfx950's
+// v_permlane32_swap swaps the two halves, so max / sum over the pair i,
+// i ^ 32 come out in every lane.
+__device__ __forceinline__ float swap16(float x) {
+  return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(x), 0x401F));  // and 0x1F, xor 0x10
+}
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Inclusive prefix sum over the 64 lanes of a wave (DPP: shifts within rows
 // of 16 lanes, then row broadcasts).
 __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {

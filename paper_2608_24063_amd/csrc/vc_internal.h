@@ -153,7 +153,29 @@ struct DecodePlan {
   const float2 *qkm, *qvm;
   const int64_t *qoff;
   const int32_t *nq;
+  // Host-built piece table (decode_step_planned only): header, then one
+  // record per workgroup.
+  const int32_t *plan;
 };
+
+// Piece table of a planned decode step.  Header words: magic, units, nwg, d,
+// max_rows, pieces, then zeros.  Record of workgroup i: unit u (-1: no
+// piece), piece j of the unit's np, the unit's first piece's slot p0 (its
+// partials use slot p0 + j), rows [r0, r1) of the unit's capacity, and the
+// unit's first pool row (low word, high word).
+constexpr int32_t kDecodePlanMagic = 0x50444356;  // "VCDP"
+constexpr int kDecodePlanHdrWords = 8;
+constexpr int kDecodePlanRecWords = 8;
+// Host: bytes of the piece table of a launch of nwg workgroups.
+inline size_t decode_plan_table_bytes(int64_t nwg) {
+  return sizeof(int32_t) * (size_t)(kDecodePlanHdrWords + kDecodePlanRecWords * nwg);
+}
+// Host: builds the piece table of `units` caches with capacities cap[] and
+// first pool rows row_off[] (host arrays) for a launch of nwg workgroups
+// (decode_grid) at head dim d and row bound max_rows.  Returns VC_OK or
+// VC_ERR_ARG (a negative capacity or offset, overlapping blocks).
+int decode_plan_build(int32_t units, const int32_t *cap, const int64_t *row_off, int64_t max_rows, int32_t nwg,
+                      int32_t d, int32_t *out);
 
 // Scratch of the allocation-free decode step (viscache_decode_step_noalloc):
 // a file-scope device array of kNoAllocBytes per device.  The arrival
@@ -172,6 +194,7 @@ hipError_t launch_append(int32_t units, int32_t d, uint16_t *k_pool, uint16_t *v
 hipError_t launch_decode(const DecodePlan &p, hipStream_t st);
 hipError_t launch_decode_step(const DecodePlan &p, hipStream_t st);
 hipError_t launch_decode_step_q4(const DecodePlan &p, hipStream_t st);
+hipError_t launch_decode_planned(const DecodePlan &p, bool q4, hipStream_t st);
 // 4-bit rows: `rows` bf16 rows of d values -> codes [rows][d/2], meta [rows][d/32].
 hipError_t launch_quant_rows(int32_t d, int64_t rows, const uint16_t *src, uint8_t *codes, float2 *meta,
                              hipStream_t st);

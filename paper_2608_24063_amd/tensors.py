@@ -7,7 +7,8 @@ import torch
 
 from . import (VC_PRUNE_EVENTS, VC_RANK_GLOBAL, make_params, make_prune_io, make_shape, prune_with_io, vc_cache,
                vc_decode_shape, vc_qcache, viscache_append_kv, viscache_budget, viscache_decode_attn,
-               viscache_decode_step, viscache_decode_step_noalloc, viscache_decode_step_q4,
+               viscache_decode_plan, viscache_decode_step, viscache_decode_step_noalloc,
+               viscache_decode_step_planned, viscache_decode_step_q4,
                viscache_decode_step_workspace_bytes,
                viscache_decode_workspace_bytes, viscache_out_rows, viscache_prune_workspace_bytes,
                viscache_quantize_rows)
@@ -183,6 +184,25 @@ class DecodeCache:
         self.nq = torch.as_tensor([int(x) for x in nq], dtype=torch.int32).to(dev)
         self.qc = vc_qcache(self.qk.data_ptr(), self.qkm.data_ptr(), self.qv.data_ptr(), self.qvm.data_ptr(),
                             self.row_off.data_ptr(), self.nq.data_ptr())
+
+    def plan(self, max_rows=None) -> None:
+        """Builds the piece table of this cache on the host
+        (viscache_decode_plan) and keeps a device copy for step_planned."""
+        self.plan_rows = self.max_cap if max_rows is None else int(max_rows)
+        blob = viscache_decode_plan(self.shape, self.caps_host, self.offs_host, self.plan_rows)
+        host = torch.frombuffer(bytearray(blob), dtype=torch.uint8)
+        self.plan_dev = host.to(self.k_pool.device)
+        self.plan_bytes = len(blob)
+
+    def step_planned(self, k_new: torch.Tensor, v_new: torch.Tensor, q: torch.Tensor, out: torch.Tensor,
+                     scale: float, q4: bool = False, max_rows=None) -> None:
+        """step() (or step_q4() with q4) over the piece table of plan()
+        (viscache_decode_step_planned)."""
+        rows = self.plan_rows if max_rows is None else int(max_rows)
+        viscache_decode_step_planned(self.shape, self.c, self.qc if q4 else None, self.plan_dev.data_ptr(),
+                                     self.plan_bytes, k_new.data_ptr(), v_new.data_ptr(), q.data_ptr(),
+                                     out.data_ptr(), scale, rows, self.step_ws.data_ptr(), self.step_ws_bytes,
+                                     _stream())
 
     def step_q4(self, k_new: torch.Tensor, v_new: torch.Tensor, q: torch.Tensor, out: torch.Tensor,
                 scale: float) -> None:

@@ -136,8 +136,68 @@ static int run_case(int idx, const std::vector<double> &v) {
     const vc_status na = viscache_decode_step_noalloc(&ds, &c, fake(905), fake(906), fake(907),
                                                       static_cast<float *>(fake(908)), 0.088f, max_rows, nullptr);
     CHECK(na == VC_ERR_HIP || (!fits && na == VC_ERR_WORKSPACE), "case %d: decode noalloc status %d", idx, (int)na);
+    // Piece table of caches holding the retained visual rows, the window and
+    // 128 generated rows per unit (every fifth unit empty), then the planned
+    // step up to its (stub) launch.
+    const int64_t units = (int64_t)L * B * Hkv;
+    std::vector<int32_t> cap((size_t)units);
+    std::vector<int64_t> off((size_t)units);
+    int64_t o = 0;
+    for (int64_t u = 0; u < units; ++u) {
+      const int b = (int)((u / Hkv) % B);
+      cap[u] = u % 5 == 4 ? 0 : (int32_t)(n[b] * p.retention) + W + 128;
+      off[u] = o;
+      o += cap[u];
+    }
+    const size_t pb = viscache_decode_plan_bytes(&ds, max_rows);
+    CHECK(pb > 0, "case %d: plan bytes", idx);
+    std::vector<int32_t> plan(pb / 4 + 1);
+    const vc_status ps = viscache_decode_plan(&ds, cap.data(), off.data(), max_rows, plan.data(), pb);
+    CHECK(ps == VC_OK, "case %d: plan status %d", idx, (int)ps);
+    if (ps == VC_OK) {
+      // Every unit's min(cap, max_rows) rows are covered once, in order, by
+      // its pieces, whose slots are p0 .. p0 + np - 1.
+      const int32_t nwg = plan[2], P = plan[5];
+      CHECK(plan[1] == units && P >= units && P <= nwg, "case %d: plan header", idx);
+      std::vector<int64_t> covered((size_t)units, 0), seen((size_t)units, 0);
+      for (int32_t i = 0; i < nwg; ++i) {
+        const int32_t *r = plan.data() + 8 + 8 * (size_t)i;
+        if (i >= P) {
+          CHECK(r[0] == -1, "case %d: record %d past the pieces", idx, i);
+          continue;
+        }
+        CHECK(r[0] >= 0 && r[0] < units && r[1] >= 0 && r[1] < r[2] && r[4] <= r[5], "case %d: record %d", idx, i);
+        if (!(r[0] >= 0 && r[0] < units)) continue;
+        covered[r[0]] += r[5] - r[4];
+        seen[r[0]] += 1;
+        CHECK(r[6] == (int32_t)(uint32_t)off[r[0]] && r[7] == (int32_t)(off[r[0]] >> 32), "case %d: offset", idx);
+      }
+      for (int64_t u = 0; u < units; ++u) {
+        const int64_t want = cap[u] < max_rows ? cap[u] : max_rows;
+        CHECK(covered[u] == want && seen[u] >= 1, "case %d: unit %lld covered %lld of %lld", idx, (long long)u,
+              (long long)covered[u], (long long)want);
+      }
+    }
+    CHECK(viscache_decode_plan(&ds, cap.data(), off.data(), max_rows, plan.data(), pb - 4) == VC_ERR_WORKSPACE,
+          "case %d: short plan buffer", idx);
+    if (units > 1 && cap[0] > 0) {
+      std::vector<int64_t> bad(off);
+      bad[1] = bad[0] + cap[0] - 1;  // overlaps unit 0's block
+      if (cap[1] > 0)
+        CHECK(viscache_decode_plan(&ds, cap.data(), bad.data(), max_rows, plan.data(), pb) == VC_ERR_ARG,
+              "case %d: overlapping blocks accepted", idx);
+    }
+    CHECK(viscache_decode_step_planned(&ds, &c, nullptr, fake(910), pb, fake(905), fake(906), fake(907),
+                                       static_cast<float *>(fake(908)), 0.088f, max_rows, fake(909), dws,
+                                       nullptr) == VC_ERR_HIP,
+          "case %d: planned step", idx);
+    CHECK(viscache_decode_step_planned(&ds, &c, nullptr, fake(910), pb - 32, fake(905), fake(906), fake(907),
+                                       static_cast<float *>(fake(908)), 0.088f, max_rows, fake(909), dws,
+                                       nullptr) == VC_ERR_ARG,
+          "case %d: planned step, short table", idx);
   } else {
     CHECK(dws == 0, "case %d: decode group above 16 accepted", idx);
+    CHECK(viscache_decode_plan_bytes(&ds, max_rows) == 0, "case %d: plan bytes for a group above 16", idx);
   }
   return 0;
 }

@@ -43,6 +43,7 @@ hipError_t launch_append(int32_t, int32_t, uint16_t *, uint16_t *, const int64_t
 hipError_t launch_decode(const DecodePlan &p, hipStream_t) { return touch(&p, sizeof(p)); }
 hipError_t launch_decode_step(const DecodePlan &p, hipStream_t) { return touch(&p, sizeof(p)); }
 hipError_t launch_decode_step_q4(const DecodePlan &p, hipStream_t) { return touch(&p, sizeof(p)); }
+hipError_t launch_decode_planned(const DecodePlan &p, bool, hipStream_t) { return touch(&p, sizeof(p)); }
 hipError_t noalloc_scratch(uint8_t **out, hipStream_t) {
   *out = nullptr;
   return hipErrorInvalidValue;

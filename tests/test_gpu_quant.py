@@ -78,11 +78,12 @@ def _attend_ref(orc, q, K, V, scale):
     return orc.attend(q, K, V, scale)
 
 
-def _q4_case(dev, orc, sg, d, Hq, Hkv, lens, nq_req, steps, seed, compact):
+def _q4_case(dev, orc, sg, d, Hq, Hkv, lens, nq_req, steps, seed, compact, planned=False):
     """Two copies of one cache: one stepped with decode_step_q4 over 4-bit
     prefixes, the other with plain decode_step.  Checks every step of the
     q4 copy against the oracle over (read-back prefix | bf16 rows) and that
-    both copies append the same rows."""
+    both copies append the same rows.  With `planned`, the q4 copy steps
+    through viscache_decode_step_planned over its piece table instead."""
     import paper_2608_24063_amd as vc
     from paper_2608_24063_amd.tensors import DecodeCache
     from synthgen.device import bf16_tensor, to_host_bf16
@@ -132,6 +133,12 @@ def _q4_case(dev, orc, sg, d, Hq, Hkv, lens, nq_req, steps, seed, compact):
             return Kd[qoff[u]:qoff[u] + n], Vd[qoff[u]:qoff[u] + n]
 
         def run(k, v, q, out, scale):
+            if planned:
+                vc.viscache_decode_step_planned(qc_cache.shape, qc_cache.c, qcs, qc_cache.plan_dev.data_ptr(),
+                                                qc_cache.plan_bytes, k.data_ptr(), v.data_ptr(), q.data_ptr(),
+                                                out.data_ptr(), scale, qc_cache.max_cap,
+                                                qc_cache.step_ws.data_ptr(), qc_cache.step_ws_bytes, stream)
+                return
             vc.viscache_decode_step_q4(qc_cache.shape, qc_cache.c, qcs, k.data_ptr(), v.data_ptr(), q.data_ptr(),
                                        out.data_ptr(), scale, qc_cache.max_cap, qc_cache.step_ws.data_ptr(),
                                        qc_cache.step_ws_bytes, stream)
@@ -149,7 +156,12 @@ def _q4_case(dev, orc, sg, d, Hq, Hkv, lens, nq_req, steps, seed, compact):
             return Kd[r0:r0 + n], Vd[r0:r0 + n]
 
         def run(k, v, q, out, scale):
-            qc_cache.step_q4(k, v, q, out, scale)
+            if planned:
+                qc_cache.step_planned(k, v, q, out, scale, q4=True)
+            else:
+                qc_cache.step_q4(k, v, q, out, scale)
+    if planned:
+        qc_cache.plan()
     scale = d ** -0.5
     cur = list(lens)
     G = Hq // Hkv
@@ -169,7 +181,7 @@ def _q4_case(dev, orc, sg, d, Hq, Hkv, lens, nq_req, steps, seed, compact):
         cur = [min(x + 1, cap) for x, cap in zip(cur, caps)]
         assert qc_cache.len.cpu().tolist() == cur == ref.len.cpu().tolist()
         assert torch.equal(qc_cache.k_pool, ref.k_pool) and torch.equal(qc_cache.v_pool, ref.v_pool)
-        if all(n == 0 for n in nq_eff):
+        if all(n == 0 for n in nq_eff) and not planned:
             assert torch.equal(out, out_r), f"step {t}: no 4-bit rows, yet differs from decode_step"
         K, V, o = to_host_bf16(qc_cache.k_pool), to_host_bf16(qc_cache.v_pool), out.cpu().numpy()
         for u in range(units):
@@ -186,24 +198,26 @@ def _q4_case(dev, orc, sg, d, Hq, Hkv, lens, nq_req, steps, seed, compact):
     return qc_cache
 
 
+@pytest.mark.parametrize("planned", [False, True])
 @pytest.mark.parametrize("d,Hq,Hkv", [(128, 8, 2), (64, 28, 4)])
-def test_decode_step_q4_compact_block(dev, orc, sg, d, Hq, Hkv):
+def test_decode_step_q4_compact_block(dev, orc, sg, d, Hq, Hkv, planned):
     """Prefixes packed in a block of their own: nq of 0, one tile, a whole
     length, more than the length (clamped), not a tile multiple (rounded
     down), and long units whose 4-bit tiles are split over workgroups."""
     units = 2 * Hkv
     lens = [64, 1023, 5000, 31, 2049, 96, 3000, 40][:units]
     nq = [0, 1000, 4992, 33, 2048, 96, 2999, 32][:units]
-    _q4_case(dev, orc, sg, d, Hq, Hkv, lens, nq, steps=3, seed=51, compact=True)
+    _q4_case(dev, orc, sg, d, Hq, Hkv, lens, nq, steps=3, seed=51, compact=True, planned=planned)
 
 
+@pytest.mark.parametrize("planned", [False, True])
 @pytest.mark.parametrize("d,Hq,Hkv", [(128, 28, 4), (64, 8, 2)])
-def test_decode_step_q4_whole_pool(dev, orc, sg, d, Hq, Hkv):
+def test_decode_step_q4_whole_pool(dev, orc, sg, d, Hq, Hkv, planned):
     """DecodeCache.quantize over the whole pool (qrow_off = row offsets)."""
     units = 2 * Hkv
     lens = [300, 4097, 33, 1024, 1, 640, 2500, 0][:units]
     nq = [288, 4096, 32, 1024, 0, 640, 2496, 0][:units]
-    _q4_case(dev, orc, sg, d, Hq, Hkv, lens, nq, steps=2, seed=61, compact=False)
+    _q4_case(dev, orc, sg, d, Hq, Hkv, lens, nq, steps=2, seed=61, compact=False, planned=planned)
 
 
 def test_decode_step_q4_without_prefix_equals_step(dev, orc, sg):

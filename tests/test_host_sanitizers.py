@@ -63,6 +63,7 @@ def test_host_code_under_sanitizers(tmp_path, sg):
     inc = ["-I", os.path.join(ROOT, "include"), "-I", "/opt/rocm/include", "-D__HIP_PLATFORM_AMD__"]
     objs = []
     for src in (os.path.join(CSRC, "vc_api.cpp"), os.path.join(CSRC, "vc_budget.cpp"),
+                os.path.join(CSRC, "vc_decode_plan.cpp"),
                 os.path.join(ROOT, "tests", "sanitize", "launch_stubs.cpp"),
                 os.path.join(ROOT, "tests", "sanitize", "host_driver.cpp")):
         obj = str(tmp_path / (os.path.basename(src) + ".o"))
