@@ -379,19 +379,26 @@ size_t viscache_decode_plan_bytes(const vc_decode_shape *shape, int64_t max_rows
  * pool rows are cap and row_off (HOST arrays of L*B*Hkv entries, the same
  * values as the vc_cache's device arrays) into `plan` (HOST, 4-byte aligned,
  * at least viscache_decode_plan_bytes bytes), for steps with this max_rows.
+ * len_hint (HOST, L*B*Hkv entries, or NULL) are the units' lengths now: the
+ * step requests each wave's first rows before it has read the unit's length,
+ * and with the hint it does so only up to 64 rows past it (rows beyond are
+ * read once the length is known), which keeps it from reading the unused
+ * end of a cache whose capacity reaches far past its length; a stale hint
+ * costs time, never correctness.
  * The caller copies the table to device memory and passes it to
  * viscache_decode_step_planned.  Each unit's min(cap, max_rows) rows are cut
  * into whole 32-row tiles; a workgroup's piece is shared by its four waves in
  * runs of consecutive tiles, and the table takes the smallest per-wave share
- * (at least two tiles) for which the pieces fit the launch.  VC_ERR_ARG for a
- * null pointer, a negative capacity or offset, negative max_rows, or units
- * whose blocks overlap; VC_ERR_UNSUPPORTED for a capacity above 2^31 - 65 or
- * a size viscache_decode_plan_bytes refuses; VC_ERR_WORKSPACE if plan_bytes
+ * (at least two tiles) for which the pieces fit the launch.  VC_ERR_ARG for
+ * a null cap, row_off or plan, a negative capacity, offset or length,
+ * negative max_rows, or units whose blocks overlap; VC_ERR_UNSUPPORTED for a
+ * capacity above 2^31 - 65 or a size viscache_decode_plan_bytes refuses;
+ * VC_ERR_WORKSPACE if plan_bytes
  * is too small.  The table stays valid while cap and row_off do not change;
  * after a change, build it again (a stale table attends the wrong rows and
  * may read outside the caches' blocks). */
 vc_status viscache_decode_plan(const vc_decode_shape *shape, const int32_t *cap, const int64_t *row_off,
-                               int64_t max_rows, void *plan, size_t plan_bytes);
+                               const int32_t *len_hint, int64_t max_rows, void *plan, size_t plan_bytes);
 
 /* Device, asynchronous.  viscache_decode_step (qcache NULL) or
  * viscache_decode_step_q4 (qcache non-NULL, as there) over the cut of a piece

@@ -94,7 +94,8 @@ def lib() -> ctypes.CDLL:
                                                    c_i64, c_vp]
         L.viscache_decode_plan_bytes.argtypes = [P(vc_decode_shape), c_i64]
         L.viscache_decode_plan_bytes.restype = ctypes.c_size_t
-        L.viscache_decode_plan.argtypes = [P(vc_decode_shape), P(c_i32), P(c_i64), c_i64, c_vp, ctypes.c_size_t]
+        L.viscache_decode_plan.argtypes = [P(vc_decode_shape), P(c_i32), P(c_i64), P(c_i32), c_i64, c_vp,
+                                           ctypes.c_size_t]
         L.viscache_decode_step_planned.argtypes = [P(vc_decode_shape), P(vc_cache), P(vc_qcache), c_vp,
                                                    ctypes.c_size_t, c_vp, c_vp, c_vp, c_vp, c_f32, c_i64, c_vp,
                                                    ctypes.c_size_t, c_vp]
@@ -273,16 +274,18 @@ def viscache_decode_plan_bytes(shape: vc_decode_shape, max_rows: int) -> int:
     return int(lib().viscache_decode_plan_bytes(ctypes.byref(shape), max_rows))
 
 
-def viscache_decode_plan(shape: vc_decode_shape, cap, row_off, max_rows: int) -> bytes:
-    """The piece table of caches with capacities `cap` and first pool rows
-    `row_off` (host sequences), built on the host; returns its bytes."""
+def viscache_decode_plan(shape: vc_decode_shape, cap, row_off, max_rows: int, len_hint=None) -> bytes:
+    """The piece table of caches with capacities `cap`, first pool rows
+    `row_off` and (optionally) current lengths `len_hint` (host sequences),
+    built on the host; returns its bytes."""
     n = len(cap)
     cap_a = (c_i32 * n)(*[int(x) for x in cap])
     off_a = (c_i64 * n)(*[int(x) for x in row_off])
+    hint_a = (c_i32 * n)(*[int(x) for x in len_hint]) if len_hint is not None else None
     nbytes = viscache_decode_plan_bytes(shape, max_rows)
     buf = (ctypes.c_int32 * max(nbytes // 4, 1))()
-    _check(lib().viscache_decode_plan(ctypes.byref(shape), cap_a, off_a, max_rows, ctypes.addressof(buf), nbytes),
-           "viscache_decode_plan")
+    _check(lib().viscache_decode_plan(ctypes.byref(shape), cap_a, off_a, hint_a, max_rows, ctypes.addressof(buf),
+                                      nbytes), "viscache_decode_plan")
     return bytes(buf)[:nbytes]
 
 

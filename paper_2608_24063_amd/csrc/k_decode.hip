@@ -447,15 +447,16 @@ struct UnitRows {
 // One wave's share of a piece: rows [a, e) of the unit, a tile at a time
 // from a (a multiple of the tile), with the next tile's rows in flight while
 // the current one is processed.  `cur` and `nxt` hold the rows of the first
-// two tiles, read by the caller (when the wave has that many, up to where
-// the caller then knew the rows end).  The wave's running (max, sum, O) of
-// the G heads come back in mrow, lsum and O.
+// two tiles, read by the caller with row indices clamped to spec - 1; a tile
+// that has rows below e at or past spec is read again (with the rows known,
+// so only when the early bound fell short).  The wave's running (max, sum,
+// O) of the G heads come back in mrow, lsum and O.
 //   S^T = K Q^T   A = K rows straight from HBM, B = Q (registers)
 //   O^T = V^T P^T A = V^T (per-wave LDS tile, transposing reads), B = P^T
 template <int D, bool Q4>
 __device__ __forceinline__ void wave_rows(const DecodePlan &p, DecodeSmem<D> &sm, const QueryOps<D, Q4> &qo,
                                           const UnitRows<D> &ur, RowTile<D> &cur, RowTile<D> &nxt, int a, int e,
-                                          int nrow, f32x4 (&O)[D / 16], float &mrow, float &lsum) {
+                                          int spec, int nrow, f32x4 (&O)[D / 16], float &mrow, float &lsum) {
   constexpr int KS = D / 32;
   constexpr int MB = D / 16;
   constexpr int PR = DecodeSmem<D>::PR;
@@ -471,9 +472,11 @@ __device__ __forceinline__ void wave_rows(const DecodePlan &p, DecodeSmem<D> &sm
   uint16_t *myvt = wave_vt(sm.wave[w]);
   const int tr_row = 4 * lg + (lr >> 2), tr_col = 4 * (lr & 3);
   const int nq = Q4 ? ur.nq : 0;
+  if (a < e && min(a + kRowTile, e) > spec) cur.load(ur.Kp, ur.Vp, a, e, lr, lg, lane);  // (bf16 only)
   for (int t0 = a; t0 < e; t0 += kRowTile) {
     const int tn = t0 + kRowTile;
-    if (t0 > a && tn < e) {  // (the second tile is in nxt already)
+    // The second tile is in nxt already, unless its early read fell short.
+    if (tn < e && (t0 > a || min(tn + kRowTile, e) > spec)) {
       if (Q4 && tn < nq)
         nxt.load_q(ur.Kc, ur.Km, ur.Vc, ur.Vm, tn, e, lr, lg, lane);
       else
@@ -599,15 +602,17 @@ __device__ __forceinline__ void finish_piece(const DecodePlan &p, DecodeSmem<D> 
   // or past G are neither output nor merged: they are skipped.
   constexpr int kEl = 16 * D / 256;
   constexpr int kHs = 256 / D;
-  const int x = tid % D, h0 = tid / D;
+  const int x = tid % D, h0 = __builtin_amdgcn_readfirstlane(tid / D);  // h0 is the same across a wave
   float2 ml[kEl][4];
   float wv[kEl][4];
 #pragma unroll
   for (int k = 0; k < kEl; ++k)
+    if (h0 + kHs * k < p.G) {  // wave-uniform
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ml[k][i] = wml[i][h0 + kHs * k];
-      wv[k][i] = reinterpret_cast<const float(*)[D + 4]>(sm.wave[i])[h0 + kHs * k][x];
+      for (int i = 0; i < 4; ++i) {
+        ml[k][i] = wml[i][h0 + kHs * k];
+        wv[k][i] = reinterpret_cast<const float(*)[D + 4]>(sm.wave[i])[h0 + kHs * k][x];
+      }
     }
   const int g = u % p.Hkv;
   const int lb_ = u / p.Hkv;
@@ -711,16 +716,20 @@ __device__ __forceinline__ void merge_pieces(const DecodePlan &p, float2 *mlb, i
     // Pair (piece j0 + t / 16, head t % 16) for t < 16 nb; the other
     // threads read pair 0 again and drop it.
     const int tp = tid < 16 * nb ? tid : 0;
-    const float *mlp = reinterpret_cast<const float *>(p.part_ml + (int64_t)(slot0 + j0) * 16 + tp);
+    const float *mlp = reinterpret_cast<const float *>(p.part_ml + (int64_t)(slot0 + j0) * 16) + 2 * tp;
     const float m0 = ld_part<COHERENT>(mlp), s0 = ld_part<COHERENT>(mlp + 1);
+    // Branch-free: pieces past the batch's end read its last piece again
+    // and are dropped below; each load is a uniform base plus the lane's
+    // 32-bit element offset.
     float po[kEl][kBatch];
 #pragma unroll
     for (int k = 0; k < kEl; ++k) {
-      if (k < nel) {
-        const float *src = p.part_o + (int64_t)(slot0 + j0) * 16 * D + min(tid + 256 * k, GD - 1);
+      if (k < nel) {  // uniform
 #pragma unroll
-        for (int b = 0; b < kBatch; ++b)
-          if (b < nb) po[k][b] = ld_part<COHERENT>(src + (int64_t)b * 16 * D);
+        for (int b = 0; b < kBatch; ++b) {
+          const float *base = p.part_o + (int64_t)(slot0 + j0 + min(b, nb - 1)) * 16 * D;
+          po[k][b] = ld_part<COHERENT>(base + min(tid + 256 * k, GD - 1));
+        }
       }
     }
     __syncthreads();  // the previous batch's pairs are read
@@ -858,7 +867,7 @@ __device__ __forceinline__ void decode_body(const DecodePlan &p) {
   if (Q4) __syncthreads();  // the query rows in LDS
   f32x4 O[D / 16];
   float mrow, lsum;
-  wave_rows<D, Q4>(p, sm, qo, ur, cur, nxt, a, e, nrow, O, mrow, lsum);
+  wave_rows<D, Q4>(p, sm, qo, ur, cur, nxt, a, e, e, nrow, O, mrow, lsum);
   if (np == 1)
     finish_piece<D, kOutput>(p, sm, u, 0, O, mrow, lsum);
   else
@@ -887,8 +896,9 @@ __device__ __forceinline__ void planned_body(const DecodePlan &p) {
   // Header and record in one round trip (both loads unconditional; the
   // host checked that the table has a record for every workgroup).
   const int h0 = ldg(hdr), h1 = ldg(hdr + 1), h2 = ldg(hdr + 2), h3 = ldg(hdr + 3), h4 = ldg(hdr + 4);
-  const int u = ldg(rec), j = ldg(rec + 1), np = ldg(rec + 2), p0 = ldg(rec + 3);
-  const int r0 = ldg(rec + 4), r1 = ldg(rec + 5);
+  const int u = ldg(rec), jn = ldg(rec + 1), p0 = ldg(rec + 2);
+  const int r0 = ldg(rec + 3), r1 = ldg(rec + 4), rs = ldg(rec + 5);
+  const int j = jn & 0xFFFF, np = jn >> 16;
   const int64_t roff = (int64_t)(((uint64_t)(uint32_t)ldg(rec + 7) << 32) | (uint32_t)ldg(rec + 6));
   // (The record's unit takes part in the check, which keeps its load beside
   // the header's instead of behind the branch.)
@@ -908,8 +918,14 @@ __device__ __forceinline__ void planned_body(const DecodePlan &p) {
   b = min(b, r1);
   // The appended row first: staging it waits for it (and for any load
   // issued before it), not for the query or the tiles.
-  const int len0 = ldg(p.len + u), capd = ldg(p.cap + u);
+  // The length and capacity as vector loads (an opaque zero offset keeps
+  // them off the scalar path, whose wait would also hold back the tile
+  // requests behind them), ahead of the tiles' requests.
+  int z;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+  const int len_v = ldg(p.len + u + z), cap_v = ldg(p.cap + u + z);
   const u32x4 nrc = load_new_chunk<D>(p, u, tid);
+  __builtin_amdgcn_sched_barrier(0);
   QueryOps<D, Q4> qo;
   qo.load(p, sm, u, w, lr, lg);
   UnitRows<D> ur{};
@@ -921,8 +937,12 @@ __device__ __forceinline__ void planned_body(const DecodePlan &p) {
     nq0 = ldg(p.nq + u);
     qoff = ldg(p.qoff + u);
   }
+  // Rows read before the length is known: up to the piece's early bound.
+  const int spec = Q4 ? 0 : min(b, rs);
   RowTile<D> cur, nxt;
-  if (!Q4) first_tiles<D, false>(ur, qo.row0, cur, nxt, a, b, lr, lg, lane);
+  if (!Q4) first_tiles<D, false>(ur, qo.row0, cur, nxt, a, spec, lr, lg, lane);
+  __builtin_amdgcn_sched_barrier(0);
+  const int len0 = __builtin_amdgcn_readfirstlane(len_v), capd = __builtin_amdgcn_readfirstlane(cap_v);
   int rows, nrow;
   unit_rows<true>(len0, capd, p.max_rows, rows, nrow);
   const int e = min(b, rows);
@@ -938,7 +958,7 @@ __device__ __forceinline__ void planned_body(const DecodePlan &p) {
   }
   f32x4 O[D / 16];
   float mrow, lsum;
-  wave_rows<D, Q4>(p, sm, qo, ur, cur, nxt, a, e, nrow, O, mrow, lsum);
+  wave_rows<D, Q4>(p, sm, qo, ur, cur, nxt, a, e, Q4 ? e : spec, nrow, O, mrow, lsum);
   if (np == 1)
     finish_piece<D, kOutput>(p, sm, u, 0, O, mrow, lsum);
   else

@@ -691,7 +691,7 @@ size_t viscache_decode_plan_bytes(const vc_decode_shape *s, int64_t max_rows) {
 }
 
 vc_status viscache_decode_plan(const vc_decode_shape *s, const int32_t *cap, const int64_t *row_off,
-                               int64_t max_rows, void *plan, size_t plan_bytes) {
+                               const int32_t *len_hint, int64_t max_rows, void *plan, size_t plan_bytes) {
   vc_status st = check_decode(s);
   if (st != VC_OK) return st;
   if (!cap || !row_off || !plan || max_rows < 0) return VC_ERR_ARG;
@@ -700,8 +700,8 @@ vc_status viscache_decode_plan(const vc_decode_shape *s, const int32_t *cap, con
   if (need == 0) return VC_ERR_UNSUPPORTED;
   if (plan_bytes < need) return VC_ERR_WORKSPACE;
   const int64_t units = (int64_t)s->L * s->B * s->Hkv;
-  return (vc_status)decode_plan_build((int32_t)units, cap, row_off, max_rows, decode_grid(units, max_rows), s->d,
-                                      static_cast<int32_t *>(plan));
+  return (vc_status)decode_plan_build((int32_t)units, cap, row_off, len_hint, max_rows, decode_grid(units, max_rows),
+                                      s->d, static_cast<int32_t *>(plan));
 }
 
 vc_status viscache_decode_step_planned(const vc_decode_shape *s, const vc_cache *c, const vc_qcache *qc,

@@ -28,15 +28,21 @@ namespace {
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// Rows past the length at planning time that the early reads still cover.
+constexpr int64_t kSpecRows = 64;
+
 // Per-wave share (tiles) of a unit of t tiles cut into np pieces.
 int64_t wave_share(int64_t t, int64_t np) { return ceil_div(ceil_div(t, np), 4); }
 
 }  // namespace
 
-int decode_plan_build(int32_t units, const int32_t *cap, const int64_t *row_off, int64_t max_rows, int32_t nwg,
-                      int32_t d, int32_t *out) {
+int decode_plan_build(int32_t units, const int32_t *cap, const int64_t *row_off, const int32_t *len_hint,
+                      int64_t max_rows, int32_t nwg, int32_t d, int32_t *out) {
   if (units < 1 || nwg <= units || max_rows < 0) return VC_ERR_ARG;
   const int64_t U = units;
+  if (len_hint)
+    for (int64_t u = 0; u < U; ++u)
+      if (len_hint[u] < 0) return VC_ERR_ARG;
   // Blocks: non-negative, and no two units' rows overlap.
   for (int64_t u = 0; u < U; ++u)
     if (cap[u] < 0 || row_off[u] < 0 || row_off[u] > INT64_MAX - cap[u]) return VC_ERR_ARG;
@@ -99,9 +105,11 @@ int decode_plan_build(int32_t units, const int32_t *cap, const int64_t *row_off,
       P += x.first;
     }
   }
+  for (int64_t u = 0; u < U; ++u)
+    if (np[u] > 0xFFFF) return VC_ERR_UNSUPPORTED;  // (at most nwg - units + 1; cannot happen)
   // Pieces in unit order (their partial slots), then dealt longest first.
   struct Pc {
-    int32_t u, j, np, p0, r0, r1, tiles;
+    int32_t u, j, np, p0, r0, r1, rs, tiles;
   };
   std::vector<Pc> pcs;
   pcs.reserve((size_t)P);
@@ -116,6 +124,9 @@ int decode_plan_build(int32_t units, const int32_t *cap, const int64_t *row_off,
       pc.p0 = (int32_t)slot;
       pc.r0 = (int32_t)(T0 * kTile);
       pc.r1 = (int32_t)std::min<int64_t>(T1 * kTile, capb[u]);
+      pc.rs = pc.r1;
+      if (len_hint)
+        pc.rs = (int32_t)std::max<int64_t>(pc.r0, std::min<int64_t>(pc.r1, (int64_t)len_hint[u] + kSpecRows));
       pc.tiles = (int32_t)(T1 - T0);
       pcs.push_back(pc);
     }
@@ -137,11 +148,11 @@ int decode_plan_build(int32_t units, const int32_t *cap, const int64_t *row_off,
       const Pc &pc = pcs[(size_t)i];
       const uint64_t ro = (uint64_t)row_off[pc.u];
       r[0] = pc.u;
-      r[1] = pc.j;
-      r[2] = pc.np;
-      r[3] = pc.p0;
-      r[4] = pc.r0;
-      r[5] = pc.r1;
+      r[1] = pc.j | (pc.np << 16);
+      r[2] = pc.p0;
+      r[3] = pc.r0;
+      r[4] = pc.r1;
+      r[5] = pc.rs;
       r[6] = (int32_t)(uint32_t)(ro & 0xFFFFFFFFu);
       r[7] = (int32_t)(uint32_t)(ro >> 32);
     } else {

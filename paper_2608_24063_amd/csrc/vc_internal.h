@@ -160,9 +160,11 @@ struct DecodePlan {
 
 // Piece table of a planned decode step.  Header words: magic, units, nwg, d,
 // max_rows, pieces, then zeros.  Record of workgroup i: unit u (-1: no
-// piece), piece j of the unit's np, the unit's first piece's slot p0 (its
-// partials use slot p0 + j), rows [r0, r1) of the unit's capacity, and the
-// unit's first pool row (low word, high word).
+// piece), piece j and the unit's piece count np (j | np << 16; np <= 512),
+// the unit's first piece's slot p0 (its partials use slot p0 + j), rows
+// [r0, r1) of the unit's capacity, the bound rs <= r1 below which rows may be
+// read before the unit's length is known, and the unit's first pool row (low
+// word, high word).
 constexpr int32_t kDecodePlanMagic = 0x50444356;  // "VCDP"
 constexpr int kDecodePlanHdrWords = 8;
 constexpr int kDecodePlanRecWords = 8;
@@ -172,10 +174,12 @@ inline size_t decode_plan_table_bytes(int64_t nwg) {
 }
 // Host: builds the piece table of `units` caches with capacities cap[] and
 // first pool rows row_off[] (host arrays) for a launch of nwg workgroups
-// (decode_grid) at head dim d and row bound max_rows.  Returns VC_OK or
-// VC_ERR_ARG (a negative capacity or offset, overlapping blocks).
-int decode_plan_build(int32_t units, const int32_t *cap, const int64_t *row_off, int64_t max_rows, int32_t nwg,
-                      int32_t d, int32_t *out);
+// (decode_grid) at head dim d and row bound max_rows; len_hint[] (host, may
+// be null) are the units' lengths when the table is built, which bound the
+// rows read early.  Returns VC_OK or VC_ERR_ARG (a negative capacity, offset
+// or length, overlapping blocks) or VC_ERR_UNSUPPORTED.
+int decode_plan_build(int32_t units, const int32_t *cap, const int64_t *row_off, const int32_t *len_hint,
+                      int64_t max_rows, int32_t nwg, int32_t d, int32_t *out);
 
 // Scratch of the allocation-free decode step (viscache_decode_step_noalloc):
 // a file-scope device array of kNoAllocBytes per device.  The arrival

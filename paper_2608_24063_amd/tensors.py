@@ -185,11 +185,19 @@ class DecodeCache:
         self.qc = vc_qcache(self.qk.data_ptr(), self.qkm.data_ptr(), self.qv.data_ptr(), self.qvm.data_ptr(),
                             self.row_off.data_ptr(), self.nq.data_ptr())
 
-    def plan(self, max_rows=None) -> None:
+    def plan(self, max_rows=None, hint=True) -> None:
         """Builds the piece table of this cache on the host
-        (viscache_decode_plan) and keeps a device copy for step_planned."""
+        (viscache_decode_plan) and keeps a device copy for step_planned.  The
+        length hint: the current lengths (hint True), none (False), or the
+        given sequence."""
         self.plan_rows = self.max_cap if max_rows is None else int(max_rows)
-        blob = viscache_decode_plan(self.shape, self.caps_host, self.offs_host, self.plan_rows)
+        if hint is True:
+            lens = self.len.cpu().tolist()
+        elif hint is False or hint is None:
+            lens = None
+        else:
+            lens = [int(x) for x in hint]
+        blob = viscache_decode_plan(self.shape, self.caps_host, self.offs_host, self.plan_rows, lens)
         host = torch.frombuffer(bytearray(blob), dtype=torch.uint8)
         self.plan_dev = host.to(self.k_pool.device)
         self.plan_bytes = len(blob)

@@ -152,7 +152,11 @@ static int run_case(int idx, const std::vector<double> &v) {
     const size_t pb = viscache_decode_plan_bytes(&ds, max_rows);
     CHECK(pb > 0, "case %d: plan bytes", idx);
     std::vector<int32_t> plan(pb / 4 + 1);
-    const vc_status ps = viscache_decode_plan(&ds, cap.data(), off.data(), max_rows, plan.data(), pb);
+    std::vector<int32_t> hint((size_t)units);
+    for (int64_t u = 0; u < units; ++u) hint[u] = cap[u] > 128 ? cap[u] - 128 : 0;
+    CHECK(viscache_decode_plan(&ds, cap.data(), off.data(), nullptr, max_rows, plan.data(), pb) == VC_OK,
+          "case %d: plan without hint", idx);
+    const vc_status ps = viscache_decode_plan(&ds, cap.data(), off.data(), hint.data(), max_rows, plan.data(), pb);
     CHECK(ps == VC_OK, "case %d: plan status %d", idx, (int)ps);
     if (ps == VC_OK) {
       // Every unit's min(cap, max_rows) rows are covered once, in order, by
@@ -166,9 +170,10 @@ static int run_case(int idx, const std::vector<double> &v) {
           CHECK(r[0] == -1, "case %d: record %d past the pieces", idx, i);
           continue;
         }
-        CHECK(r[0] >= 0 && r[0] < units && r[1] >= 0 && r[1] < r[2] && r[4] <= r[5], "case %d: record %d", idx, i);
+        const int32_t j = r[1] & 0xFFFF, npc = r[1] >> 16;
+        CHECK(r[0] >= 0 && r[0] < units && j < npc && r[3] <= r[5] && r[5] <= r[4], "case %d: record %d", idx, i);
         if (!(r[0] >= 0 && r[0] < units)) continue;
-        covered[r[0]] += r[5] - r[4];
+        covered[r[0]] += r[4] - r[3];
         seen[r[0]] += 1;
         CHECK(r[6] == (int32_t)(uint32_t)off[r[0]] && r[7] == (int32_t)(off[r[0]] >> 32), "case %d: offset", idx);
       }
@@ -178,13 +183,14 @@ static int run_case(int idx, const std::vector<double> &v) {
               (long long)covered[u], (long long)want);
       }
     }
-    CHECK(viscache_decode_plan(&ds, cap.data(), off.data(), max_rows, plan.data(), pb - 4) == VC_ERR_WORKSPACE,
+    CHECK(viscache_decode_plan(&ds, cap.data(), off.data(), hint.data(), max_rows, plan.data(), pb - 4) ==
+              VC_ERR_WORKSPACE,
           "case %d: short plan buffer", idx);
     if (units > 1 && cap[0] > 0) {
       std::vector<int64_t> bad(off);
       bad[1] = bad[0] + cap[0] - 1;  // overlaps unit 0's block
       if (cap[1] > 0)
-        CHECK(viscache_decode_plan(&ds, cap.data(), bad.data(), max_rows, plan.data(), pb) == VC_ERR_ARG,
+        CHECK(viscache_decode_plan(&ds, cap.data(), bad.data(), nullptr, max_rows, plan.data(), pb) == VC_ERR_ARG,
               "case %d: overlapping blocks accepted", idx);
     }
     CHECK(viscache_decode_step_planned(&ds, &c, nullptr, fake(910), pb, fake(905), fake(906), fake(907),

@@ -11,14 +11,19 @@ import paper_2608_24063_amd as vc
 TILE = 32
 
 
-def _table(shape, cap, off, max_rows):
-    blob = vc.viscache_decode_plan(shape, cap, off, max_rows)
+def _table(shape, cap, off, max_rows, hint=None):
+    """Header and records, the records unpacked to (u, j, np, p0, r0, r1, rs,
+    first pool row)."""
+    blob = vc.viscache_decode_plan(shape, cap, off, max_rows, hint)
     a = np.frombuffer(blob, dtype=np.int32)
-    return a[:8], a[8:].reshape(-1, 8)
+    r = a[8:].reshape(-1, 8).astype(np.int64)
+    rec = np.stack([r[:, 0], r[:, 1] & 0xFFFF, r[:, 1] >> 16, r[:, 2], r[:, 3], r[:, 4], r[:, 5],
+                    (r[:, 7] << 32) | (r[:, 6] & 0xFFFFFFFF)], axis=1)
+    return a[:8], rec
 
 
-def _check(shape, cap, off, max_rows):
-    hdr, rec = _table(shape, cap, off, max_rows)
+def _check(shape, cap, off, max_rows, hint=None):
+    hdr, rec = _table(shape, cap, off, max_rows, hint)
     units = shape.L * shape.B * shape.Hkv
     nwg, P = int(hdr[2]), int(hdr[5])
     assert hdr[0] == 0x50444356 and hdr[1] == units and hdr[3] == shape.d and hdr[4] == min(max_rows, 2**31 - 1)
@@ -40,8 +45,11 @@ def _check(shape, cap, off, max_rows):
         assert mine[0, 4] == 0 and mine[-1, 5] == capb[u]
         assert np.all(mine[1:, 4] == mine[:-1, 5]), f"unit {u}: pieces not contiguous"
         assert np.all(mine[:, 4] % TILE == 0)
-        ro = (mine[:, 7].astype(np.int64) << 32) | (mine[:, 6].astype(np.int64) & 0xFFFFFFFF)
-        assert np.all(ro == off[u])
+        assert np.all(mine[:, 7] == off[u])
+        # The early-read bound: within the piece, and at the hint plus 64
+        # rows (or the piece's end without a hint).
+        want = mine[:, 5] if hint is None else np.clip(hint[u] + 64, mine[:, 4], mine[:, 5])
+        assert np.all(mine[:, 6] == want), f"unit {u}: early bound {mine[:, 6]} != {want}"
     assert sorted(slots) == list(range(P)), "partial slots are not 0 .. P-1 once each"
     # Longest first.
     ptiles = -(-(live[:, 5] - live[:, 4]) // TILE)
@@ -82,6 +90,7 @@ def test_plan_on_pruned_workload_caches(sg, case):
                 caps.append(int(k[b * w.L + l]) + w.W + 128)
     cap, off = _caps_offs(caps)
     _check(shape, cap, off, max(cap))
+    _check(shape, cap, off, max(cap), [c - 128 for c in cap])
 
 
 def test_plan_edges():
@@ -93,8 +102,10 @@ def test_plan_edges():
         if trial % 3 == 0:
             caps[5] = 100000
         cap, off = _caps_offs(caps)
+        hint = [int(x) for x in rng.integers(0, 3100, size=16)]
         for max_rows in (max(cap), 0, 1, 33, 4096):
             _check(shape, cap, off, max_rows)
+            _check(shape, cap, off, max_rows, hint)
     # A single huge unit (many pieces), and all units empty.
     _check(vc.vc_decode_shape(1, 1, 8, 1, 64), [200000], [0], 200000)
     _check(shape, [0] * 16, [0] * 16, 0)
@@ -118,6 +129,9 @@ def test_plan_refusals():
         vc.viscache_decode_plan(shape, cap, [0, 10, -20, 30], 10)
     assert e.value.status == vc.VC_ERR_ARG
     with pytest.raises(vc.VisCacheError) as e:
+        vc.viscache_decode_plan(shape, cap, off, 10, [3, -1, 0, 0])  # negative length
+    assert e.value.status == vc.VC_ERR_ARG
+    with pytest.raises(vc.VisCacheError) as e:
         vc.viscache_decode_plan(shape, [2**31 - 64, 1, 1, 1], [0, 2**31, 2**31 + 1, 2**31 + 2], 2**31 - 64)
     assert e.value.status == vc.VC_ERR_UNSUPPORTED
     with pytest.raises(vc.VisCacheError) as e:
@@ -131,7 +145,7 @@ def test_plan_refusals():
     ca = (ctypes.c_int32 * 4)(*cap)
     oa = (ctypes.c_int64 * 4)(*off)
     L = vc.lib()
-    assert (L.viscache_decode_plan(ctypes.byref(shape), ca, oa, 10, ctypes.addressof(buf), n - 4)
+    assert (L.viscache_decode_plan(ctypes.byref(shape), ca, oa, None, 10, ctypes.addressof(buf), n - 4)
             == vc.VC_ERR_WORKSPACE)
-    assert L.viscache_decode_plan(ctypes.byref(shape), ca, oa, 10, None, n) == vc.VC_ERR_ARG
-    assert L.viscache_decode_plan(ctypes.byref(shape), ca, oa, 10, ctypes.addressof(buf), n) == vc.VC_OK
+    assert L.viscache_decode_plan(ctypes.byref(shape), ca, oa, None, 10, None, n) == vc.VC_ERR_ARG
+    assert L.viscache_decode_plan(ctypes.byref(shape), ca, oa, None, 10, ctypes.addressof(buf), n) == vc.VC_OK

@@ -64,14 +64,17 @@ def _step_unplanned(c, kt, vt, qt, out, scale, max_rows):
                             max_rows, c.step_ws.data_ptr(), c.step_ws_bytes, torch.cuda.current_stream().cuda_stream)
 
 
-@pytest.mark.parametrize("d,Hq,Hkv,max_rows", [(128, 8, 2, None), (64, 28, 4, None), (128, 64, 8, None),
-                                               (128, 28, 4, 2000)])
-def test_planned_step_random_caches(dev, orc, sg, d, Hq, Hkv, max_rows):
+@pytest.mark.parametrize("d,Hq,Hkv,max_rows,hint", [(128, 8, 2, None, "now"), (64, 28, 4, None, "none"),
+                                                    (128, 64, 8, None, "now"), (128, 28, 4, 2000, "now"),
+                                                    (128, 8, 2, None, "stale"), (64, 28, 4, None, "stale")])
+def test_planned_step_random_caches(dev, orc, sg, d, Hq, Hkv, max_rows, hint):
     """Lengths on and around tile edges, empty units, units cut into many
     pieces, capacities with no room, little room and much room (a long NaN
     tail that the first tiles read before the length is known), five steps:
     the same lengths and pools as viscache_decode_step, and every head of
-    every unit against the oracle at every step."""
+    every unit against the oracle at every step.  The table's length hint is
+    the lengths now, none (early reads up to the capacity), or stale (500
+    rows short: the early reads fall short and are read again)."""
     from paper_2608_24063_amd.tensors import DecodeCache
     from synthgen.device import bf16_tensor, to_host_bf16
     L, B = 2, 2
@@ -93,7 +96,7 @@ def test_planned_step_random_caches(dev, orc, sg, d, Hq, Hkv, max_rows):
     Vp = sg.normal_bf16(81, 2, (c.total_rows, d))
     for cc in (c, a):
         _fill(cc, Kp, Vp, lens, dev)
-    c.plan(rows)
+    c.plan(rows, hint={"now": True, "none": False, "stale": [max(0, n - 500) for n in lens]}[hint])
     scale = d ** -0.5
     G = Hq // Hkv
     cur = list(lens)
