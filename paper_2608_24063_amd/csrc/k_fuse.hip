@@ -326,13 +326,18 @@ __device__ __forceinline__ void fuse_job(const PrunePlan &p, const u32x4 (&rec)[
 #pragma unroll
     for (int it = 0; it < kIt; ++it) pend[it] = di[3][it];
   }
+  // Rows past the job's end get zero operands.  The select reads every
+  // kept-value register here, after the wait for tile 0 (loaded after them),
+  // so no wait on these loads is left for the tile loop, where it would
+  // stall on the newest prefetches instead.
   bool kvalid[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     kvalid[nb] = w * 32 + nb * 16 + lr < nrows;
-    if (!kvalid[nb]) {
 #pragma unroll
-      for (int s = 0; s < KS; ++s) st.bvk[nb][s] = as_bf16x8(u32x4{0, 0, 0, 0});
+    for (int s = 0; s < KS; ++s) {
+      const u32x4 v = as_u32x4(st.bvk[nb][s]);
+      st.bvk[nb][s] = as_bf16x8(kvalid[nb] ? v : u32x4{0, 0, 0, 0});
     }
   }
   __syncthreads();
