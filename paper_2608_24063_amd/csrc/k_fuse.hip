@@ -11,9 +11,10 @@
 //   O^T = V_d^T P^T     A = V_d^T (LDS, transposing reads),   B = P^T (registers)
 // so the scores' accumulator layout (lane: kept row l%16, dropped rows
 // 4*(l/16)+i) is directly the B operand of the second product, and each lane
-// ends holding kept row l%16, columns 16*mb + 4*(l/16) + i -- the same columns
-// it loaded of V_k, which the mu-blend reuses.  With fp32 output the
-// probabilities enter the second product as a bf16 hi + lo pair.
+// ends holding kept row l%16, columns 16*mb + 4*(l/16) + i; the mu-blend
+// takes V_k at those columns from its operand registers through LDS.  With
+// fp32 output the probabilities enter the second product as a bf16 hi + lo
+// pair.
 //
 // Pipeline per workgroup: dropped-row indices are fetched four tiles ahead,
 // the rows themselves three tiles ahead into two register sets, and staged
@@ -318,6 +319,9 @@ __device__ __forceinline__ void fuse_job(const PrunePlan &p, const u32x4 (&rec)[
     if (c / kCpr < nrows)
       st16(boff<uint16_t>(Kout, (uint32_t)(j0 + c / kCpr) * kRowBytes + 16u * (c % kCpr)), kc[i]);
   }
+  // The previous job's waves may still read their kept values from the
+  // tile buffers (below): nothing is staged before every wave is past them.
+  __syncthreads();
   if (ntiles > 0) {
     set0.store(vr[0], row0, chunk);
     int rr[kIt];
@@ -389,6 +393,25 @@ __device__ __forceinline__ void fuse_job(const PrunePlan &p, const u32x4 (&rec)[
   }
   next();
 
+  // Every wave is past its last tile (the take synchronises), so the tile
+  // buffers are free: each wave moves its kept values from the operand
+  // layout (row l % 16, columns 32 s + 8 lg ..) to the output layout
+  // (columns 16 mb + 4 lg ..) through its own 32 rows of a 128-row table at
+  // the tile pitch, instead of reading them from memory again.
+  constexpr int PR = kPitchRow<D>;
+  uint16_t *kvt = &vr[0][0];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      *reinterpret_cast<u32x4 *>(kvt + (w * 32 + nb * 16 + lr) * PR + 32 * s + 8 * lg) = as_u32x4(st.bvk[nb][s]);
+  u32x2 kvv[NB][MB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+      kvv[nb][mb] = *reinterpret_cast<const u32x2 *>(kvt + (w * 32 + nb * 16 + lr) * PR + 16 * mb + 4 * lg);
+
   const float mu = p.mu, omu = 1.f - p.mu;
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
@@ -398,14 +421,9 @@ __device__ __forceinline__ void fuse_job(const PrunePlan &p, const u32x4 (&rec)[
     if (!kvalid[nb]) continue;
     const float inv = (r > 0 && ls > 0.f) ? 1.f / ls : 0.f;
     const uint32_t orow_j = (uint32_t)(j0 + w * 32 + nb * 16 + lr);
-    // Kept values at this lane's output columns 16 mb + 4 lg + i (L2-hot).
-    const uint32_t vrow = (uint32_t)clampi(kv_idx[nb]) * kRowBytes + 8u * lg;
-    u32x2 kvv[MB];
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) kvv[mb] = ld8(boff<const uint16_t>(Vin, vrow + 32u * mb));
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
-      const uint32_t w0 = kvv[mb].x, w1 = kvv[mb].y;
+      const uint32_t w0 = kvv[nb][mb].x, w1 = kvv[nb][mb].y;
       const float vk[4] = {bf16_lo(w0), bf16_hi(w0), bf16_lo(w1), bf16_hi(w1)};
       float o[4];
 #pragma unroll
