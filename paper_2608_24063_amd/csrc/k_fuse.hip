@@ -396,9 +396,11 @@ __device__ __forceinline__ void fuse_job(const PrunePlan &p, const u32x4 (&rec)[
   // Every wave is past its last tile (the take synchronises), so the tile
   // buffers are free: each wave moves its kept values from the operand
   // layout (row l % 16, columns 32 s + 8 lg ..) to the output layout
-  // (columns 16 mb + 4 lg ..) through its own 32 rows of a 128-row table at
-  // the tile pitch, instead of reading them from memory again.
-  constexpr int PR = kPitchRow<D>;
+  // (columns 16 mb + 4 lg ..) through its own 32 rows of a 128-row table,
+  // instead of reading them from memory again.  At a pitch of D + 8
+  // elements the 16-byte writes and the 8-byte reads are conflict-free.
+  constexpr int PR = D + 8;
+  static_assert(128 * PR <= 2 * kDropTile * kPitchRow<D>, "the kept-value table fits the tile buffers");
   uint16_t *kvt = &vr[0][0];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb)
