@@ -10,12 +10,15 @@
 // least 2 tiles: below that a split saves less than the merge of its pieces
 // costs) for which splitting every unit into ceil(tiles / 4m) pieces fits
 // the launch's workgroups; workgroups left over then split further the units
-// that need the fewest extra pieces to bring their share below m.  Pieces are
-// dealt to workgroups longest first, so a launch with more pieces than
-// resident slots starts its longest ones first, and consecutive workgroups
-// (which the hardware spreads over the XCDs) carry similar loads.
+// that need the fewest extra pieces to bring their share below m.  With more
+// units than resident slots whose units past the first round are short, no
+// unit is cut (see below).  Pieces are dealt to workgroups longest first, so
+// a launch with more pieces than resident slots starts its longest ones
+// first, and consecutive workgroups (which the hardware spreads over the
+// XCDs) carry similar loads.
 #include <algorithm>
 #include <cstdint>
+#include <functional>
 #include <numeric>
 #include <vector>
 
@@ -82,7 +85,19 @@ int decode_plan_build(int32_t units, const int32_t *cap, const int64_t *row_off,
     else
       lo = mid + 1;
   }
-  const int64_t m = lo;
+  int64_t m = lo;
+  // More units than resident slots: if the units past the first round are
+  // at most a quarter of the longest (they fill the gaps the first round
+  // leaves), cut none, since a split only adds its merge; otherwise the
+  // longest would wait for a second round whole, and the cut above
+  // shortens them.
+  bool cut_none = false;
+  if (U > kDecodeSlots) {
+    std::vector<int64_t> ts(t);
+    std::nth_element(ts.begin(), ts.begin() + kDecodeSlots, ts.end(), std::greater<int64_t>());
+    cut_none = 4 * ts[(size_t)kDecodeSlots] <= tmax;
+    if (cut_none) m = std::max(m, ceil_div(tmax, 4));
+  }
   std::vector<int64_t> np((size_t)U);
   int64_t P = 0;
   for (int64_t u = 0; u < U; ++u) {
@@ -90,8 +105,8 @@ int decode_plan_build(int32_t units, const int32_t *cap, const int64_t *row_off,
     P += np[u];
   }
   // Leftover workgroups: bring the units whose share is m below it, those
-  // needing the fewest extra pieces first.
-  if (m > m_lo && P < nwg) {
+  // needing the fewest extra pieces first (not when no unit is to be cut).
+  if (!cut_none && m > m_lo && P < nwg) {
     std::vector<std::pair<int64_t, int64_t>> need;  // (extra pieces, unit)
     for (int64_t u = 0; u < U; ++u)
       if (wave_share(t[u], np[u]) >= m) need.emplace_back(ceil_div(t[u], 4 * (m - 1)) - np[u], u);

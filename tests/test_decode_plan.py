@@ -56,7 +56,8 @@ def _check(shape, cap, off, max_rows, hint=None):
     assert np.all(np.diff(ptiles) <= 0)
     # The per-wave share: a piece of n tiles gives its waves ceil(n / 4); the
     # largest over pieces is the smallest (at least 2) for which splitting
-    # every unit into ceil(tiles / 4m) pieces fits the grid.
+    # every unit into ceil(tiles / 4m) pieces fits the grid, unless no unit
+    # is to be cut (below).
     share = int(max(1, (-(-ptiles // 4)).max()))
 
     def pieces(m):
@@ -65,7 +66,13 @@ def _check(shape, cap, off, max_rows, hint=None):
     m = 2
     while pieces(m) > nwg:
         m += 1
-    assert share <= max(m, 1), f"share {share} above the smallest fitting bound {m}"
+    # More units than the 512 resident slots, and the units past the first
+    # round at most a quarter of the longest: no unit is cut.
+    ts = np.sort(tiles)[::-1]
+    if units > 512 and 4 * ts[512] <= ts[0]:
+        assert P == units, f"{P} pieces for {units} units where none should be cut"
+    else:
+        assert share <= max(m, 1), f"share {share} above the smallest fitting bound {m}"
     return hdr, rec
 
 
@@ -114,6 +121,20 @@ def test_plan_edges():
     off = [1000 - 64 * i for i in range(16)]
     off = [int(x) for x in np.argsort(off) * 100]
     _check(shape, cap, off, 64)
+
+
+def test_plan_more_units_than_slots():
+    """Past 512 units (the resident slots) no unit is cut when the units past
+    the first round are at most a quarter of the longest; else the usual cut."""
+    shape = vc.vc_decode_shape(1, 75, 8, 8, 128)  # 600 units
+    caps = [2048] * 500 + [128] * 100
+    cap, off = _caps_offs(caps)
+    hdr, rec = _check(shape, cap, off, max(cap))
+    assert int(hdr[5]) == 600
+    caps = [2048] * 600
+    cap, off = _caps_offs(caps)
+    hdr, rec = _check(shape, cap, off, max(cap))
+    assert int(hdr[5]) > 600
 
 
 def test_plan_refusals():
