@@ -4,6 +4,8 @@
 //   stats : per row r, the max m_r and sum_v exp(z_rv - m_r) over a key split
 //   colsum: combines the splits, then S[v] = sum_r exp(z_rv - m_r) / sum_r
 // and, for the shared ranking, a fixed-order fp64 sum over layers and heads.
+#include <type_traits>
+
 #include "vc_device.h"
 #include "vc_internal.h"
 
@@ -48,6 +50,17 @@ struct TileRegs {
       const int row = c / (D / 8), col = c % (D / 8);
       const int64_t gr = r0 + row;
       v[i] = gr < rmax ? ld16(src + gr * D + col * 8) : u32x4{0, 0, 0, 0};
+    }
+  }
+  // Rows clamped to rmax - 1 instead of zeroed (no branch, so waits on
+  // later loads stay exact); the callers mask rows past rmax.
+  __device__ __forceinline__ void load_clamped(const uint16_t *src, int64_t r0, int64_t rmax, int tid) {
+#pragma unroll
+    for (int i = 0; i < kChunks; ++i) {
+      const int c = tid + i * 256;
+      const int row = c / (D / 8), col = c % (D / 8);
+      const int64_t gr = min(r0 + row, rmax - 1);
+      v[i] = ld16(src + gr * D + col * 8);
     }
   }
   __device__ __forceinline__ void store(uint16_t *lds, int tid) const {
@@ -242,24 +255,35 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p, uint32_t *p
   for (int qb = 0; qb < 4; ++qb) { m[qb] = kFloor; sum[qb] = 0.f; }
 
   const int ntiles = (k1 - k0 + kKeyTile - 1) / kKeyTile;
-  TileRegs<D> tr;
+  // Tile j travels in register set j & 1: it is loaded at the top of
+  // iteration j - 2 and staged at the end of iteration j - 1.
+  TileRegs<D> tr0, tr1;
   if (ntiles > 0) {
-    tr.load(K, k0, k1, tid);
-    tr.store(kt[0], tid);
+    tr0.load_clamped(K, k0, k1, tid);
+    tr1.load_clamped(K, min(k0 + kKeyTile, k1 - 1), k1, tid);
+    tr0.store(kt[0], tid);
   }
   __syncthreads();
-  for (int t = 0; t < ntiles; ++t) {
+  auto step = [&](auto par, int t) {
+    constexpr int PAR = decltype(par)::value;
+    TileRegs<D> &cur = PAR ? tr1 : tr0, &nxt = PAR ? tr0 : tr1;
     const int tb = k0 + t * kKeyTile;
-    if (t + 1 < ntiles) tr.load(K, tb + kKeyTile, k1, tid);
+    cur.load_clamped(K, min(tb + 2 * kKeyTile, k1 - 1), k1, tid);  // tile t + 2 (past the end: never staged)
     if (active) {
       if (tb + kKeyTile <= k1)
-        stats_tile<D, false>(kt[t & 1], bq, m, sum, tb, k1, lr, lg, sc);
+        stats_tile<D, false>(kt[PAR], bq, m, sum, tb, k1, lr, lg, sc);
       else
-        stats_tile<D, true>(kt[t & 1], bq, m, sum, tb, k1, lr, lg, sc);
+        stats_tile<D, true>(kt[PAR], bq, m, sum, tb, k1, lr, lg, sc);
     }
-    if (t + 1 < ntiles) tr.store(kt[(t + 1) & 1], tid);
+    if (t + 1 < ntiles) nxt.store(kt[PAR ^ 1], tid);
     __syncthreads();
+  };
+  int t = 0;
+  for (; t + 1 < ntiles; t += 2) {
+    step(std::integral_constant<int, 0>{}, t);
+    step(std::integral_constant<int, 1>{}, t + 1);
   }
+  if (t < ntiles) step(std::integral_constant<int, 0>{}, t);
 
   if (!active) return;
 
