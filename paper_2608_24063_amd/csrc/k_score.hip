@@ -74,6 +74,47 @@ struct TileRegs {
   }
 };
 
+
+#define VC_LDS_AS __attribute__((address_space(3)))
+
+// A 64-row tile of bf16 rows in LDS, filled by direct global-to-LDS loads
+// (no staging registers): each 16-byte load instruction of a wave writes
+// 1 KB of LDS, lane i bytes [16i, 16i + 16).  Row r keeps its 16-byte chunk c
+// at slot c ^ sw(r), so the 16 rows one operand read touches fall on 16
+// distinct bank groups.
+template <int D>
+struct RowTileLds {
+  static constexpr int kSlots = D / 8;                 // 16-byte chunks per row
+  static constexpr int kLoadsPerWave = 64 * D * 2 / 1024 / 4;
+  static constexpr int kRowsPerLoad = 1024 / (D * 2);
+  __device__ static __forceinline__ int sw(int r) { return (r * kSlots / 16) & (kSlots - 1); }
+  // This wave's share of rows r0 .. r0 + 63; rows at or past rmax repeat
+  // row rmax - 1 (callers give them no weight).
+  __device__ static __forceinline__ void issue(const uint16_t *src, int r0, int rmax, uint16_t *buf, int w,
+                                               int lane) {
+#pragma unroll
+    for (int j = 0; j < kLoadsPerWave; ++j) {
+      const int ld = w * kLoadsPerWave + j;
+      const int r = ld * kRowsPerLoad + lane / kSlots;
+      const int c = (lane % kSlots) ^ sw(r);
+      const uint16_t *s = src + (int64_t)min(r0 + r, rmax - 1) * D + c * 8;
+      __builtin_amdgcn_global_load_lds((const VC_GLOBAL void *)s, (VC_LDS_AS void *)(buf + ld * 512), 16, 0, 0);
+    }
+  }
+  // Operand of rows rb*16 + lr, k-elements 32*s + 8*lg .. + 8.
+  __device__ static __forceinline__ bf16x8 operand(const uint16_t *buf, int rb, int s, int lr, int lg) {
+    const int r = rb * 16 + lr;
+    return as_bf16x8(*reinterpret_cast<const u32x4 *>(buf + r * D + ((4 * s + lg) ^ sw(r)) * 8));
+  }
+};
+
+// Barrier after which the direct loads this wave issued have landed in LDS.
+__device__ __forceinline__ void lds_fill_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0); expcnt and lgkmcnt left alone
+  __syncthreads();
+}
+
 __device__ __forceinline__ void unit_coords(const PrunePlan &p, int u, int &ls, int &b, int &g) {
   g = u % p.Hkv;
   b = (u / p.Hkv) % p.B;
@@ -308,17 +349,18 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p, uint32_t *p
 // ---------------------------------------------------------------------------
 // Pass 2: column sums.  Workgroup = (unit, 256-key chunk).  Wave w owns keys
 // chunk*256 + w*64 + [0, 64) as B operands; the G*W query rows (bf16 copies
-// written by pass 1) stream through LDS 64 rows at a time as A operands, so the
+// written by pass 1) stream through LDS 64 rows at a time as A operands (direct
+// global-to-LDS loads into a chunk-swizzled tile, one tile ahead), so the
 // product is Z (queries x keys): lane l sees key l%16 of each 16-key block and
 // rows 4*(l/16)+i, and accumulates exp2(z*sc - m_r) / sum_r per key.
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256, 3) void k_score_colsum(PrunePlan p) {
   constexpr int KS = D / 32;
-  constexpr int P = kPitch<D>;
   constexpr int kMaxR = 1024;
-  __shared__ __attribute__((aligned(16))) uint16_t qt[2][64 * P];
+  __shared__ __attribute__((aligned(16))) uint16_t qt[2][64 * D];
   __shared__ __attribute__((aligned(16))) float2 rs[kMaxR];
+  using QT = RowTileLds<D>;
 
   const uint32_t lb = xcd_block(blockIdx.x, gridDim.x);
   const int c = lb % p.ncol;
@@ -350,8 +392,7 @@ __global__ __launch_bounds__(256, 3) void k_score_colsum(PrunePlan p) {
     for (int s = 0; s < KS; ++s)
       bk[kb][s] = as_bf16x8(key < n ? ld16(K + (int64_t)key * D + 32 * s + 8 * lg) : u32x4{0, 0, 0, 0});
   }
-  TileRegs<D> tr;
-  tr.load(Qb, 0, R, tid);
+  QT::issue(Qb, 0, R, qt[0], w, lane);
 
   // Row statistics: merge the key splits of pass 1.  Rows past R get a
   // reference of +inf so they contribute exp2(-inf) = 0.
@@ -377,15 +418,15 @@ __global__ __launch_bounds__(256, 3) void k_score_colsum(PrunePlan p) {
     }
     rs[r] = st;
   }
-  tr.store(qt[0], tid);
-  __syncthreads();
+  lds_fill_barrier();
 
   float col[4] = {0.f, 0.f, 0.f, 0.f};
   const int ntiles = Rpad / 64;
-  for (int t = 0; t < ntiles; ++t) {
-    if (t + 1 < ntiles) tr.load(Qb, (t + 1) * 64, R, tid);
+  auto step = [&](auto par, int t) {
+    constexpr int PAR = decltype(par)::value;
+    if (t + 1 < ntiles) QT::issue(Qb, (t + 1) * 64, R, qt[PAR ^ 1], w, lane);
     if (active) {
-      const uint16_t *ql = qt[t & 1];
+      const uint16_t *ql = qt[PAR];
       // Two halves of two query blocks x four key blocks: eight accumulation
       // chains at a time, every operand read from LDS feeding four products.
 #pragma unroll
@@ -395,8 +436,7 @@ __global__ __launch_bounds__(256, 3) void k_score_colsum(PrunePlan p) {
         for (int s = 0; s < KS; ++s) {
           bf16x8 a[2];
 #pragma unroll
-          for (int q2 = 0; q2 < 2; ++q2)
-            a[q2] = as_bf16x8(*reinterpret_cast<const u32x4 *>(ql + ((2 * qh + q2) * 16 + lr) * P + 32 * s + 8 * lg));
+          for (int q2 = 0; q2 < 2; ++q2) a[q2] = QT::operand(ql, 2 * qh + q2, s, lr, lg);
 #pragma unroll
           for (int q2 = 0; q2 < 2; ++q2)
 #pragma unroll
@@ -418,9 +458,14 @@ __global__ __launch_bounds__(256, 3) void k_score_colsum(PrunePlan p) {
         }
       }
     }
-    if (t + 1 < ntiles) tr.store(qt[(t + 1) & 1], tid);
-    __syncthreads();
+    lds_fill_barrier();
+  };
+  int t = 0;
+  for (; t + 1 < ntiles; t += 2) {
+    step(std::integral_constant<int, 0>{}, t);
+    step(std::integral_constant<int, 1>{}, t + 1);
   }
+  if (t < ntiles) step(std::integral_constant<int, 0>{}, t);
   if (!active) return;
 
   float *S = p.S + (int64_t)ls * p.Ntot * p.Hkv + toff * p.Hkv + (int64_t)g * n;
