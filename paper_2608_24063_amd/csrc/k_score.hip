@@ -21,11 +21,6 @@ constexpr float kNegInf = -__builtin_inff();
 // underflows to 0 and exp2(floor - floor) is 1.
 constexpr float kFloor = -1e30f;
 
-// LDS row pitch of staged K / Q tiles: 32 bytes of padding keeps rows 16-byte
-// aligned and measured free of bank conflicts for the 16-byte operand reads.
-template <int D>
-constexpr int kPitch = D + 16;
-
 // Interleave hints for the scheduler: alternate one matrix instruction with
 // `v` vector instructions, `n` times.
 template <int n, int v>
@@ -36,44 +31,6 @@ __device__ __forceinline__ void interleave_mfma_valu() {
     __builtin_amdgcn_sched_group_barrier(0x002, v, 0);
   }
 }
-
-// A tile of 64 rows x D bf16 staged through registers into LDS; rows past
-// `rmax` read as zero.  The whole workgroup (256 threads) participates.
-template <int D>
-struct TileRegs {
-  static constexpr int kChunks = 64 * D / 8 / 256;  // 16-byte chunks per thread
-  u32x4 v[kChunks];
-  __device__ __forceinline__ void load(const uint16_t *src, int64_t r0, int64_t rmax, int tid) {
-#pragma unroll
-    for (int i = 0; i < kChunks; ++i) {
-      const int c = tid + i * 256;
-      const int row = c / (D / 8), col = c % (D / 8);
-      const int64_t gr = r0 + row;
-      v[i] = gr < rmax ? ld16(src + gr * D + col * 8) : u32x4{0, 0, 0, 0};
-    }
-  }
-  // Rows clamped to rmax - 1 instead of zeroed (no branch, so waits on
-  // later loads stay exact); the callers mask rows past rmax.
-  __device__ __forceinline__ void load_clamped(const uint16_t *src, int64_t r0, int64_t rmax, int tid) {
-#pragma unroll
-    for (int i = 0; i < kChunks; ++i) {
-      const int c = tid + i * 256;
-      const int row = c / (D / 8), col = c % (D / 8);
-      const int64_t gr = min(r0 + row, rmax - 1);
-      v[i] = ld16(src + gr * D + col * 8);
-    }
-  }
-  __device__ __forceinline__ void store(uint16_t *lds, int tid) const {
-    constexpr int P = kPitch<D>;
-#pragma unroll
-    for (int i = 0; i < kChunks; ++i) {
-      const int c = tid + i * 256;
-      const int row = c / (D / 8), col = c % (D / 8);
-      *reinterpret_cast<u32x4 *>(lds + row * P + col * 8) = v[i];
-    }
-  }
-};
-
 
 #define VC_LDS_AS __attribute__((address_space(3)))
 
@@ -115,6 +72,17 @@ __device__ __forceinline__ void lds_fill_barrier() {
   __syncthreads();
 }
 
+// The same, leaving this wave's newest N (< 16) vector memory operations in
+// flight: the direct loads of later tiles, when nothing else was issued after
+// them.
+template <int N>
+__device__ __forceinline__ void lds_fill_barrier_but() {
+  static_assert(N >= 0 && N < 16, "vmcnt field");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);  // vmcnt(N); expcnt and lgkmcnt left alone
+  __syncthreads();
+}
+
 __device__ __forceinline__ void unit_coords(const PrunePlan &p, int u, int &ls, int &b, int &g) {
   g = u % p.Hkv;
   b = (u / p.Hkv) % p.B;
@@ -124,7 +92,8 @@ __device__ __forceinline__ void unit_coords(const PrunePlan &p, int u, int &ls, 
 // ---------------------------------------------------------------------------
 // Pass 1: row statistics.  Workgroup = (unit, 256-row query group, key split).
 // Wave w owns query rows qg*256 + w*64 + [0, 64) as MFMA B operands and all
-// four waves share each 64-key tile of K staged in LDS (A operands), so the
+// four waves share each 64-key tile of K in LDS (A operands; direct loads into
+// a ring of three chunk-swizzled tiles, two ahead of the one in use), so the
 // product is Z^T (keys x queries): lane l sees query l%16 of each 16-row block
 // and keys 4*(l/16)+i, and keeps a running (max, sum) per query in registers.
 // ---------------------------------------------------------------------------
@@ -175,13 +144,11 @@ __device__ __forceinline__ void stats_tile(const uint16_t *kl, const bf16x8 (&bq
                                            float (&m)[4], float (&sum)[4], int tb, int k1, int lr,
                                            int lg, float sc) {
   constexpr int KS = D / 32;
-  constexpr int P = kPitch<D>;
   bf16x8 a[4][KS];
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-    for (int s = 0; s < KS; ++s)
-      a[kb][s] = as_bf16x8(*reinterpret_cast<const u32x4 *>(kl + (kb * 16 + lr) * P + 32 * s + 8 * lg));
+    for (int s = 0; s < KS; ++s) a[kb][s] = RowTileLds<D>::operand(kl, kb, s, lr, lg);
   f32x4 cur[4], nxt[4];
 #pragma unroll
   for (int s = 0; s < KS; ++s)
@@ -215,8 +182,10 @@ __device__ __forceinline__ uint64_t chunk_u64(const UploadChunk<CW> &c, int w) {
 template <int D, uint32_t CW>
 __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p, uint32_t *plan_dst, UploadChunk<CW> c) {
   constexpr int KS = D / 32;
-  constexpr int P = kPitch<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t kt[2][kKeyTile * P];
+  // K tiles through a ring of three LDS buffers (direct loads, chunk
+  // swizzled), two in flight ahead of the one in use.
+  __shared__ __attribute__((aligned(16))) uint16_t kt[3][kKeyTile * D];
+  using KT = RowTileLds<D>;
 
   for (uint32_t i = blockIdx.x * 256 + threadIdx.x; i < c.words; i += gridDim.x * 256) plan_dst[i] = c.data[i];
 
@@ -296,35 +265,36 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p, uint32_t *p
   for (int qb = 0; qb < 4; ++qb) { m[qb] = kFloor; sum[qb] = 0.f; }
 
   const int ntiles = (k1 - k0 + kKeyTile - 1) / kKeyTile;
-  // Tile j travels in register set j & 1: it is loaded at the top of
-  // iteration j - 2 and staged at the end of iteration j - 1.
-  TileRegs<D> tr0, tr1;
+  // Tile t lives in buffer t % 3: it is requested at step t - 2 (into the
+  // buffer tile t - 3 left, which every wave is past) and waited for at the
+  // end of step t - 1, with tile t + 1's loads left in flight.  Tiles past
+  // the end re-read the last key and are never used.
   if (ntiles > 0) {
-    tr0.load_clamped(K, k0, k1, tid);
-    tr1.load_clamped(K, min(k0 + kKeyTile, k1 - 1), k1, tid);
-    tr0.store(kt[0], tid);
+    KT::issue(K, k0, k1, kt[0], w, lane);
+    KT::issue(K, min(k0 + kKeyTile, k1 - 1), k1, kt[1], w, lane);
+    lds_fill_barrier_but<KT::kLoadsPerWave>();
   }
-  __syncthreads();
   auto step = [&](auto par, int t) {
     constexpr int PAR = decltype(par)::value;
-    TileRegs<D> &cur = PAR ? tr1 : tr0, &nxt = PAR ? tr0 : tr1;
     const int tb = k0 + t * kKeyTile;
-    cur.load_clamped(K, min(tb + 2 * kKeyTile, k1 - 1), k1, tid);  // tile t + 2 (past the end: never staged)
+    KT::issue(K, min(tb + 2 * kKeyTile, k1 - 1), k1, kt[(PAR + 2) % 3], w, lane);
     if (active) {
       if (tb + kKeyTile <= k1)
         stats_tile<D, false>(kt[PAR], bq, m, sum, tb, k1, lr, lg, sc);
       else
         stats_tile<D, true>(kt[PAR], bq, m, sum, tb, k1, lr, lg, sc);
     }
-    if (t + 1 < ntiles) nxt.store(kt[PAR ^ 1], tid);
-    __syncthreads();
+    lds_fill_barrier_but<KT::kLoadsPerWave>();
   };
   int t = 0;
-  for (; t + 1 < ntiles; t += 2) {
+  for (; t + 2 < ntiles; t += 3) {
     step(std::integral_constant<int, 0>{}, t);
     step(std::integral_constant<int, 1>{}, t + 1);
+    step(std::integral_constant<int, 2>{}, t + 2);
   }
   if (t < ntiles) step(std::integral_constant<int, 0>{}, t);
+  if (t + 1 < ntiles) step(std::integral_constant<int, 1>{}, t + 1);
+  if (ntiles > 0) lds_fill_barrier();  // every load in flight lands before the workgroup's LDS is released
 
   if (!active) return;
 
