@@ -84,6 +84,17 @@ __device__ __forceinline__ void tile_barrier() {
   __syncthreads();
 }
 
+// Scheduling hint: one matrix instruction, then `v` vector instructions,
+// `n` times.
+template <int n, int v>
+__device__ __forceinline__ void interleave_mfma_valu() {
+#pragma unroll
+  for (int i = 0; i < n; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, v, 0);
+  }
+}
+
 // Token position of the row `off` (< 64) rows after a row at position base.
 __device__ __forceinline__ int run_pos(int base, int off, int N) {
   if (N >= 64) {
@@ -186,59 +197,84 @@ __global__ __launch_bounds__(256, 2) void k_pscore(PrunePlan p, uint32_t *plan_d
       if (t + 1 < ntA) KT::issue(Kv, Kt, n, tb + 64, kend, kt[(t + 1) & 1], w, lane);
       if (active) {
         const uint16_t *kl = kt[t & 1];
-        const bool interior = tb + 63 <= wmin;  // wave-uniform
         // Two halves of 32 keys (operands of one half in registers at a time);
-        // each half updates the rows' running max and sum.
+        // each half updates the rows' running max and sum.  Tiles wholly at or
+        // before every row of the wave take the copy without the causal mask,
+        // so no branch separates a block's products from the softmax they
+        // overlap with.
+        auto tileA = [&](auto intr) {
+          constexpr bool INTERIOR = decltype(intr)::value;
 #pragma unroll
-        for (int kh = 0; kh < 2; ++kh) {
-          bf16x8 a[2][KS];
-#pragma unroll
-          for (int k2 = 0; k2 < 2; ++k2)
-#pragma unroll
-            for (int s = 0; s < KS; ++s) a[k2][s] = KT::operand(kl, 2 * kh + k2, s, lr, lg);
-#pragma unroll
-          for (int qb = 0; qb < 4; ++qb) {
-            f32x4 acc[2];
-#pragma unroll
-            for (int s = 0; s < KS; ++s)
-#pragma unroll
-              for (int k2 = 0; k2 < 2; ++k2)
-                acc[k2] = mfma_bf16(a[k2][s], bq[qb][s], s == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : acc[k2]);
-            if (!interior) {
-              // Keys past the row's token (this covers keys past kend too).
-#pragma unroll
-              for (int k2 = 0; k2 < 2; ++k2)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                  if (tb + (2 * kh + k2) * 16 + 4 * lg + i > pos[qb]) acc[k2][i] = kNegInf;
-            }
-            // Exponentials against the running max as it stands; only when
-            // they grow past 2^96 (the row's first keys, or a logit far above
-            // the earlier ones) is the max raised and the half redone.
-            float part = 0.f;
+          for (int kh = 0; kh < 2; ++kh) {
+            bf16x8 a[2][KS];
 #pragma unroll
             for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
-              for (int i = 0; i < 4; ++i) part += fast_exp2(fmaf(acc[k2][i], sc, -m[qb]));
-            if (part <= 0x1p96f) {
-              sum[qb] += part;
-            } else {
-              float tm = kNegInf;
+              for (int s = 0; s < KS; ++s) a[k2][s] = KT::operand(kl, 2 * kh + k2, s, lr, lg);
+            // The products of block qb + 1 are issued ahead of the softmax of
+            // block qb, so the matrix and vector work overlap.
+            auto prod = [&](int qb, f32x4 (&acc)[2]) {
+#pragma unroll
+              for (int s = 0; s < KS; ++s)
+#pragma unroll
+                for (int k2 = 0; k2 < 2; ++k2)
+                  acc[k2] = mfma_bf16(a[k2][s], bq[qb][s], s == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : acc[k2]);
+            };
+            f32x4 cur[2], nxt[2];
+            prod(0, cur);
+#pragma unroll
+            for (int qb = 0; qb < 4; ++qb) {
+              if (INTERIOR && qb + 1 < 4) prod(qb + 1, nxt);
+              f32x4 (&acc)[2] = cur;
+              if constexpr (!INTERIOR) {
+                // Keys past the row's token (this covers keys past kend too).
+#pragma unroll
+                for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+                  for (int i = 0; i < 4; ++i)
+                    if (tb + (2 * kh + k2) * 16 + 4 * lg + i > pos[qb]) acc[k2][i] = kNegInf;
+              }
+              // Exponentials against the running max as it stands; only when
+              // they grow past 2^96 (the row's first keys, or a logit far above
+              // the earlier ones) is the max raised and the half redone.
+              float part = 0.f;
 #pragma unroll
               for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) tm = fmaxf(tm, acc[k2][i]);
-              const float mnew = fmaxf(m[qb], tm * sc);
-              part = 0.f;
+                for (int i = 0; i < 4; ++i) part += fast_exp2(fmaf(acc[k2][i], sc, -m[qb]));
+              if (part <= 0x1p96f) {
+                sum[qb] += part;
+              } else {
+                float tm = kNegInf;
 #pragma unroll
-              for (int k2 = 0; k2 < 2; ++k2)
+                for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) part += fast_exp2(fmaf(acc[k2][i], sc, -mnew));
-              sum[qb] = fmaf(sum[qb], fast_exp2(m[qb] - mnew), part);
-              m[qb] = mnew;
+                  for (int i = 0; i < 4; ++i) tm = fmaxf(tm, acc[k2][i]);
+                const float mnew = fmaxf(m[qb], tm * sc);
+                part = 0.f;
+#pragma unroll
+                for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+                  for (int i = 0; i < 4; ++i) part += fast_exp2(fmaf(acc[k2][i], sc, -mnew));
+                sum[qb] = fmaf(sum[qb], fast_exp2(m[qb] - mnew), part);
+                m[qb] = mnew;
+              }
+              if (qb + 1 < 4) {
+                if constexpr (INTERIOR) {
+                  interleave_mfma_valu<2 * KS, 3>();
+#pragma unroll
+                  for (int k2 = 0; k2 < 2; ++k2) cur[k2] = nxt[k2];
+                } else {
+                  prod(qb + 1, cur);
+                }
+              }
             }
           }
-        }
+        };
+        if (tb + 63 <= wmin)  // wave-uniform
+          tileA(std::true_type{});
+        else
+          tileA(std::false_type{});
       }
       tile_barrier();
     }
