@@ -114,7 +114,11 @@ template <int D, uint32_t CW>
 __global__ __launch_bounds__(256, 2) void k_pscore(PrunePlan p, uint32_t *plan_dst, UploadChunk<CW> c) {
   constexpr int KS = D / 32;
   using KT = KTile<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t kt[2][64 * D];
+  // The two key tiles are separate LDS variables: the compiler then knows
+  // that a direct load into one does not write the other, and does not drain
+  // the next tile's loads before reading the current one.
+  __shared__ __attribute__((aligned(16))) uint16_t kt0[64 * D];
+  __shared__ __attribute__((aligned(16))) uint16_t kt1[64 * D];
   __shared__ __attribute__((aligned(16))) float lse[kStatsRows];  // per row: max*sc + log2(sum); +inf: none
   __shared__ float cs[2][4][64];     // per key tile: the four waves' column sums
 
@@ -189,14 +193,15 @@ __global__ __launch_bounds__(256, 2) void k_pscore(PrunePlan p, uint32_t *plan_d
     float m[4], sum[4];
 #pragma unroll
     for (int qb = 0; qb < 4; ++qb) { m[qb] = kFloor; sum[qb] = 0.f; }
-    KT::issue(Kv, Kt, n, 0, kend, kt[0], w, lane);
+    KT::issue(Kv, Kt, n, 0, kend, kt0, w, lane);
     tile_barrier();
-    for (int t = 0; t < ntA; ++t) {
+    auto stepA = [&](auto par, int t) {
+      constexpr int PAR = decltype(par)::value;
       const int tb = t * 64;
       // The other buffer was last read in tile t - 1, before the last barrier.
-      if (t + 1 < ntA) KT::issue(Kv, Kt, n, tb + 64, kend, kt[(t + 1) & 1], w, lane);
+      if (t + 1 < ntA) KT::issue(Kv, Kt, n, tb + 64, kend, PAR ? kt0 : kt1, w, lane);
       if (active) {
-        const uint16_t *kl = kt[t & 1];
+        const uint16_t *kl = PAR ? kt1 : kt0;
         // Two halves of 32 keys (operands of one half in registers at a time);
         // each half updates the rows' running max and sum.  Tiles wholly at or
         // before every row of the wave take the copy without the causal mask,
@@ -277,6 +282,14 @@ __global__ __launch_bounds__(256, 2) void k_pscore(PrunePlan p, uint32_t *plan_d
           tileA(std::false_type{});
       }
       tile_barrier();
+    };
+    {
+      int t = 0;
+      for (; t + 1 < ntA; t += 2) {
+        stepA(std::integral_constant<int, 0>{}, t);
+        stepA(std::integral_constant<int, 1>{}, t + 1);
+      }
+      if (t < ntA) stepA(std::integral_constant<int, 0>{}, t);
     }
     // Combine the four lane groups of each row; publish max*sc + log2(sum).
     if (active) {
@@ -296,23 +309,24 @@ __global__ __launch_bounds__(256, 2) void k_pscore(PrunePlan p, uint32_t *plan_d
     // ---------------- pass B: column sums over the visual keys 0 .. min(kend, n)-1
     const int kendB = min(kend, n);
     const int ntB = (kendB + 63) / 64;
-    KT::issue(Kv, Kt, n, 0, kendB, kt[0], w, lane);
+    KT::issue(Kv, Kt, n, 0, kendB, kt0, w, lane);
     tile_barrier();  // also publishes lse
     float pend = 0.f;  // tid < 64: the column partial of the tile in flight, read ahead
-    for (int t = 0; t < ntB; ++t) {
+    auto stepB = [&](auto par, int t) {
+      constexpr int PAR = decltype(par)::value;
       const int tb = t * 64;
-      if (t + 1 < ntB) KT::issue(Kv, Kt, n, tb + 64, kendB, kt[(t + 1) & 1], w, lane);
+      if (t + 1 < ntB) KT::issue(Kv, Kt, n, tb + 64, kendB, PAR ? kt0 : kt1, w, lane);
       if (tid < 64) {
         // The previous tile's column sums are complete since the last barrier.
         if (t > 0 && tb - 64 + tid < n) {
-          const int pb = (t - 1) & 1;
+          constexpr int pb = PAR ^ 1;
           stg(cp + tb - 64 + tid, pend + ((cs[pb][0][tid] + cs[pb][1][tid]) + (cs[pb][2][tid] + cs[pb][3][tid])));
         }
         pend = tb + tid < n ? ldg(cp + tb + tid) : 0.f;
       }
       float col[4] = {0.f, 0.f, 0.f, 0.f};
       if (active) {
-        const uint16_t *kl = kt[t & 1];
+        const uint16_t *kl = PAR ? kt1 : kt0;
         const bool interior = tb + 63 <= wmin;  // wave-uniform
 #pragma unroll
         for (int kh = 0; kh < 2; ++kh) {
@@ -359,15 +373,23 @@ __global__ __launch_bounds__(256, 2) void k_pscore(PrunePlan p, uint32_t *plan_d
       }
       if (lg == 0) {
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) cs[t & 1][w][kb * 16 + lr] = col[kb];
+        for (int kb = 0; kb < 4; ++kb) cs[PAR][w][kb * 16 + lr] = col[kb];
       }
       tile_barrier();
+    };
+    {
+      int t = 0;
+      for (; t + 1 < ntB; t += 2) {
+        stepB(std::integral_constant<int, 0>{}, t);
+        stepB(std::integral_constant<int, 1>{}, t + 1);
+      }
+      if (t < ntB) stepB(std::integral_constant<int, 0>{}, t);
     }
     if (tid < 64 && (ntB - 1) * 64 + tid < n) {
       const int pb = (ntB - 1) & 1;
       stg(cp + (ntB - 1) * 64 + tid, pend + ((cs[pb][0][tid] + cs[pb][1][tid]) + (cs[pb][2][tid] + cs[pb][3][tid])));
     }
-    // The next group writes kt[0], lse and cs only after barriers that every
+    // The next group writes kt0, lse and cs only after barriers that every
     // read above precedes.
   }
 }

@@ -74,13 +74,18 @@ __device__ __forceinline__ void lds_fill_barrier() {
 
 // The same, leaving this wave's newest N (< 16) vector memory operations in
 // flight: the direct loads of later tiles, when nothing else was issued after
-// them.
+// them.  A plain s_barrier, not __syncthreads(): the latter's release fence
+// counts those loads as pending LDS writes and waits for all of them.  The
+// wait here covers what the fence would: the older direct loads (vmcnt) and
+// every LDS access of this wave (lgkmcnt); the empty asm statements keep the
+// compiler from moving memory accesses across the barrier.
 template <int N>
 __device__ __forceinline__ void lds_fill_barrier_but() {
   static_assert(N >= 0 && N < 16, "vmcnt field");
   asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt(0x0F70 | N);  // vmcnt(N); expcnt and lgkmcnt left alone
-  __syncthreads();
+  __builtin_amdgcn_s_waitcnt(0x0070 | N);  // vmcnt(N) lgkmcnt(0); expcnt left alone
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
 __device__ __forceinline__ void unit_coords(const PrunePlan &p, int u, int &ls, int &b, int &g) {
@@ -184,7 +189,15 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p, uint32_t *p
   constexpr int KS = D / 32;
   // K tiles through a ring of three LDS buffers (direct loads, chunk
   // swizzled), two in flight ahead of the one in use.
-  __shared__ __attribute__((aligned(16))) uint16_t kt[3][kKeyTile * D];
+  // Separate LDS variables, so the compiler knows a direct load into one
+  // tile does not write the others and leaves the later tiles in flight.
+  __shared__ __attribute__((aligned(16))) uint16_t kt0[kKeyTile * D];
+  __shared__ __attribute__((aligned(16))) uint16_t kt1[kKeyTile * D];
+  __shared__ __attribute__((aligned(16))) uint16_t kt2[kKeyTile * D];
+  auto ktile = [&](auto i) -> uint16_t * {
+    constexpr int I = decltype(i)::value;
+    return I == 0 ? kt0 : I == 1 ? kt1 : kt2;
+  };
   using KT = RowTileLds<D>;
 
   for (uint32_t i = blockIdx.x * 256 + threadIdx.x; i < c.words; i += gridDim.x * 256) plan_dst[i] = c.data[i];
@@ -270,19 +283,19 @@ __global__ __launch_bounds__(256, 2) void k_score_stats(PrunePlan p, uint32_t *p
   // end of step t - 1, with tile t + 1's loads left in flight.  Tiles past
   // the end re-read the last key and are never used.
   if (ntiles > 0) {
-    KT::issue(K, k0, k1, kt[0], w, lane);
-    KT::issue(K, min(k0 + kKeyTile, k1 - 1), k1, kt[1], w, lane);
+    KT::issue(K, k0, k1, kt0, w, lane);
+    KT::issue(K, min(k0 + kKeyTile, k1 - 1), k1, kt1, w, lane);
     lds_fill_barrier_but<KT::kLoadsPerWave>();
   }
   auto step = [&](auto par, int t) {
     constexpr int PAR = decltype(par)::value;
     const int tb = k0 + t * kKeyTile;
-    KT::issue(K, min(tb + 2 * kKeyTile, k1 - 1), k1, kt[(PAR + 2) % 3], w, lane);
+    KT::issue(K, min(tb + 2 * kKeyTile, k1 - 1), k1, ktile(std::integral_constant<int, (PAR + 2) % 3>{}), w, lane);
     if (active) {
       if (tb + kKeyTile <= k1)
-        stats_tile<D, false>(kt[PAR], bq, m, sum, tb, k1, lr, lg, sc);
+        stats_tile<D, false>(ktile(par), bq, m, sum, tb, k1, lr, lg, sc);
       else
-        stats_tile<D, true>(kt[PAR], bq, m, sum, tb, k1, lr, lg, sc);
+        stats_tile<D, true>(ktile(par), bq, m, sum, tb, k1, lr, lg, sc);
     }
     lds_fill_barrier_but<KT::kLoadsPerWave>();
   };
@@ -328,7 +341,8 @@ template <int D>
 __global__ __launch_bounds__(256, 3) void k_score_colsum(PrunePlan p) {
   constexpr int KS = D / 32;
   constexpr int kMaxR = 1024;
-  __shared__ __attribute__((aligned(16))) uint16_t qt[2][64 * D];
+  __shared__ __attribute__((aligned(16))) uint16_t qt0[64 * D];  // separate variables: see the statistics pass
+  __shared__ __attribute__((aligned(16))) uint16_t qt1[64 * D];
   __shared__ __attribute__((aligned(16))) float2 rs[kMaxR];
   using QT = RowTileLds<D>;
 
@@ -362,7 +376,7 @@ __global__ __launch_bounds__(256, 3) void k_score_colsum(PrunePlan p) {
     for (int s = 0; s < KS; ++s)
       bk[kb][s] = as_bf16x8(key < n ? ld16(K + (int64_t)key * D + 32 * s + 8 * lg) : u32x4{0, 0, 0, 0});
   }
-  QT::issue(Qb, 0, R, qt[0], w, lane);
+  QT::issue(Qb, 0, R, qt0, w, lane);
 
   // Row statistics: merge the key splits of pass 1.  Rows past R get a
   // reference of +inf so they contribute exp2(-inf) = 0.
@@ -394,9 +408,9 @@ __global__ __launch_bounds__(256, 3) void k_score_colsum(PrunePlan p) {
   const int ntiles = Rpad / 64;
   auto step = [&](auto par, int t) {
     constexpr int PAR = decltype(par)::value;
-    if (t + 1 < ntiles) QT::issue(Qb, (t + 1) * 64, R, qt[PAR ^ 1], w, lane);
+    if (t + 1 < ntiles) QT::issue(Qb, (t + 1) * 64, R, PAR ? qt0 : qt1, w, lane);
     if (active) {
-      const uint16_t *ql = qt[PAR];
+      const uint16_t *ql = PAR ? qt1 : qt0;
       // Two halves of two query blocks x four key blocks: eight accumulation
       // chains at a time, every operand read from LDS feeding four products.
 #pragma unroll
